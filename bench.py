@@ -1,0 +1,266 @@
+"""Benchmark of the MoE-layer hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload dsv3]
+
+A step is one moe_layer call (gate, route, dispatch, grouped expert FFN,
+shared expert on a second stream, combine) over the workload's T tokens, with
+inputs and weights already resident in HBM. Prints ONE JSON line: tokens/s of
+the layer, the roofline of the dominant kernel pair (the grouped expert FFN,
+timed with HIP events on its own stream), and the CPU oracle timed on a
+bounded sample of the same workload as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix cores
+METRIC = "MoE layer tokens/s at DeepSeek-V3 shape; % bf16 MFMA peak / % HBM BW"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic(p: dict, counts) -> dict:
+    """Algorithmic bytes and flops (activated experts only, each byte once)."""
+    T, d, E, k, I = p["T"], p["d"], p["E"], p["k"], p["I"]
+    es = 2 if p["dtype"] == "bf16" else 4
+    touched = int((counts > 0).sum())
+    w_expert = 3 * I * d * es
+    ffn_bytes = touched * w_expert + T * d * es + T * k * d * es       # weights + x in + y_perm out
+    ffn_flops = 6.0 * T * k * d * I
+    Is = p.get("I_shared", 0) if p.get("n_shared", 0) else 0
+    layer_bytes = touched * w_expert + 3 * Is * d * es + E * d * es + 2 * T * d * es
+    layer_flops = 2.0 * T * d * E + ffn_flops + 6.0 * T * d * Is
+    return dict(touched_experts=touched, ffn_bytes=ffn_bytes, ffn_flops=ffn_flops, layer_bytes=layer_bytes,
+                layer_flops=layer_flops, bytes_per_expert=w_expert)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("gemm_bf16.hip",):
+        with open(os.path.join(ROOT, "paper_2603_02376_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per expert-FFN call from the rocprofv3 counter runs committed
+    under profiles/, or None when absent or taken on another kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_expert_ffn_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_call")
+
+
+def run_workload(name: str, steps: int, warmup: int, want_cpu: bool):
+    import numpy as np
+    import torch
+
+    from paper_2603_02376_amd import inputs, moe
+
+    p = inputs.preset(name)
+    cfg = moe.MoeConfig(d=p["d"], E=p["E"], k=p["k"], I=p["I"], n_groups=p["n_groups"],
+                        topk_groups=p["topk_groups"], n_shared=p["n_shared"], I_shared=p["I_shared"],
+                        score=p["score"], renorm=p["renorm"], scale=p["scale"], dtype=p["dtype"])
+    T = p["T"]
+    log(f"[bench] {name}: generating inputs on device")
+    t = inputs.make_inputs(p, 0, "cuda")
+    ws = moe.alloc_workspace(cfg, T)
+    out = torch.empty((T, p["d"]), dtype=cfg.torch_dtype, device="cuda")
+    s_main = torch.cuda.current_stream()
+    s_aux = torch.cuda.Stream()
+
+    def layer(dbg=None):
+        moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], t["w_gate"], t["w_up"], t["w_down"],
+                      t["ws_gate"], t["ws_up"], t["ws_down"], out, ws, s_main=s_main, s_aux=s_aux, dbg=dbg)
+
+    # untimed call that exports the routing, for the algorithmic byte count
+    dbg = dict(counts=torch.empty(p["E"], dtype=torch.int32, device="cuda"),
+               offsets=torch.empty(p["E"] + 1, dtype=torch.int32, device="cuda"),
+               sorted_token=torch.empty(T * p["k"], dtype=torch.int32, device="cuda"),
+               topk_idx=torch.empty((T, p["k"]), dtype=torch.int32, device="cuda"),
+               topk_w=torch.empty((T, p["k"]), dtype=torch.float32, device="cuda"),
+               logits=torch.empty((T, p["E"]), dtype=torch.float32, device="cuda"))
+    layer(dbg)
+    torch.cuda.synchronize()
+    counts = dbg["counts"].cpu().numpy()
+    alg = algorithmic(p, counts)
+
+    for _ in range(warmup):
+        layer()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"[bench] {name}: timing {steps} layer steps")
+    wall0 = time.perf_counter()
+    e0.record(s_main)
+    for _ in range(steps):
+        layer()
+    e1.record(s_main)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = e0.elapsed_time(e1) / steps
+
+    # dominant kernel pair: the grouped expert FFN, timed alone on its stream
+    y = torch.empty((T * p["k"], p["d"]), dtype=cfg.torch_dtype, device="cuda")
+
+    def ffn():
+        moe.moe_expert_ffn(cfg, T, t["x"], dbg["sorted_token"], dbg["offsets"], t["w_gate"], t["w_up"],
+                           t["w_down"], y, ws, stream=s_main)
+
+    for _ in range(max(2, warmup)):
+        ffn()
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record(s_main)
+    for _ in range(steps):
+        ffn()
+    f1.record(s_main)
+    torch.cuda.synchronize()
+    ffn_ms = f0.elapsed_time(f1) / steps
+
+    res = dict(
+        name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms,
+        counts_max_over_mean=float(counts.max() / counts.mean()), empty_experts=int((counts == 0).sum()),
+        layer_hbm_frac=alg["layer_bytes"] / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
+        layer_mfma_frac=alg["layer_flops"] / (ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12),
+        ffn_gbs=alg["ffn_bytes"] / (ffn_ms / 1e3) / 1e9,
+        ffn_tflops=alg["ffn_flops"] / (ffn_ms / 1e3) / 1e12,
+    )
+    if want_cpu:
+        res["cpu"] = cpu_baseline(p, t)
+    del t, ws, out, y
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(p, t, n_tokens: int = 16):
+    """The oracle, as it stands, on the first n_tokens tokens of the workload:
+    gate logits, routing, every selected expert's SwiGLU FFN, shared expert and
+    combine, all in fp64 on the host cores. The weights of the experts those
+    tokens use are copied to host memory before the clock starts."""
+    import numpy as np
+
+    from oracle import moe_oracle as O
+    from paper_2603_02376_amd import inputs
+
+    rows = np.arange(min(n_tokens, p["T"]))
+    x = inputs.oracle_view(t["x"])
+    wr = inputs.oracle_view(t["w_router"])
+    bias = None if p["score"] == "softmax" else inputs.oracle_view(t["bias"])
+    # experts the sample needs: route once before the clock starts, copy their weights to host RAM
+    kw = dict(k=p["k"], score=p["score"], bias=bias, n_groups=p["n_groups"], topk_groups=p["topk_groups"],
+              renorm=p["renorm"], scale=p["scale"])
+    need = np.unique(O.route(O.gate_logits(x[rows], wr), **kw)[0])
+    host_w = {n: {int(e): inputs.oracle_view(t[n][int(e)]) for e in need} for n in ("w_gate", "w_up", "w_down")}
+    sh = [inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")] if p["n_shared"] else [None] * 3
+
+    t0 = time.perf_counter()
+    logits = O.gate_logits(x[rows], wr)
+    idx, w = O.route(logits, **kw)
+    O.layer_rows(x, rows, idx, w, host_w["w_gate"], host_w["w_up"], host_w["w_down"], *sh)
+    dt = time.perf_counter() - t0
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=None)
+    except Exception:
+        pass
+    return dict(value=len(rows) / dt, unit="tokens/s", cores=threads or len(os.sched_getaffinity(0)),
+                kind="oracle", seconds=dt,
+                sample=f"first {len(rows)} of {p['T']} tokens of the {p.get('name')} workload: gate, routing, "
+                       f"{len(need)} routed experts' SwiGLU FFN{', shared expert' if p['n_shared'] else ''} "
+                       f"and combine in fp64 (weights pre-copied to host RAM)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dsv3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the mixtral and decode side measurements")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the layer is one GPU's share of the "
+              "expert-parallel MoE layer and no multi-GPU path is built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2603_02376_amd import moe
+
+    moe.lib()  # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)
+    extra = {}
+    if not args.no_extra:
+        for name in ("dsv3_decode", "mixtral"):
+            if name == args.workload:
+                continue
+            r = run_workload(name, args.steps, args.warmup, False)
+            extra[name] = dict(tokens_per_s=round(r["tokens_per_s"], 1), ms_per_step=round(r["ms"], 4),
+                               layer_hbm_frac=round(r["layer_hbm_frac"], 4),
+                               layer_mfma_frac=round(r["layer_mfma_frac"], 4),
+                               expert_ffn_ms=round(r["ffn_ms"], 4), expert_ffn_gbs=round(r["ffn_gbs"], 1),
+                               expert_ffn_tflops=round(r["ffn_tflops"], 1))
+
+    r = main_res
+    p = r["p"]
+    alg = r["alg"]
+    hbm_bound = alg["ffn_flops"] / alg["ffn_bytes"] < (MFMA_BF16_PEAK_TFLOPS * 1e12) / (HBM_PEAK_GBS * 1e9)
+    if hbm_bound:
+        roof = dict(bound="hbm", achieved=round(r["ffn_gbs"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(r["ffn_gbs"] / HBM_PEAK_GBS, 4))
+    else:
+        roof = dict(bound="mfma", achieved=round(r["ffn_tflops"], 1), peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                    frac=round(r["ffn_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4))
+    roof["traffic"] = measured_traffic(args.workload)
+    roof.update(kernel="moe_expert_ffn: grouped GEMM1+SwiGLU and grouped GEMM2 (2 launches per call)",
+                ms_per_call=round(r["ffn_ms"], 4), algorithmic_bytes=alg["ffn_bytes"],
+                algorithmic_flops=alg["ffn_flops"], touched_experts=alg["touched_experts"])
+    out = {
+        "metric": METRIC,
+        "value": round(r["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": p["dtype"],
+        "data": "synthetic (seeded; random-init weights of the workload's shape)",
+        "config": {"workload": (f"{args.workload}: T={p['T']} d={p['d']} E={p['E']} top-{p['k']}"
+                                + (f" (top-{p['topk_groups']} of {p['n_groups']} groups)" if p["n_groups"] > 1 else "")
+                                + f" I={p['I']}" + (f" + shared I={p['I_shared']}" if p["n_shared"] else "")),
+                   "global_batch": p["T"], "parallelism": "single GPU (one GPU's share of expert parallelism)"},
+        "layer_hbm_frac": round(r["layer_hbm_frac"], 4),
+        "layer_mfma_frac": round(r["layer_mfma_frac"], 4),
+        "routing": {"max_over_mean_load": round(r["counts_max_over_mean"], 3), "empty_experts": r["empty_experts"]},
+        "roofline": roof,
+    }
+    if "cpu" in r:
+        out["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r["cpu"].items()}
+    if extra:
+        out["extra"] = extra
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,209 @@
+/*
+ * moe.h — C ABI of the MI355X (gfx950) MoE-layer library (libmoe.so).
+ *
+ * The library runs one GPU's share of the DeepSeek-V3 Mixture-of-Experts layer
+ * that the paper reproduces (App. M, "DeepSeek-V3 MoE Dispatch and Combine";
+ * §4 Workloads; the host pipeline listing in App. F): gating and top-k
+ * routing, dispatch of tokens to experts, the per-expert SwiGLU FFN
+ * (GEMM1 gate/up projection, SwiGLU, GEMM2 down projection) and the weighted
+ * combine. On one GPU the dispatch and combine all-to-alls of the paper become
+ * an on-device permutation and its inverse. The paper does not define the
+ * gate, scores, top-k rule or combine weights; the library implements the
+ * public DeepSeek-V3 rule (sigmoid scores, selection bias, group-limited
+ * top-k, normalised and scaled weights) and the Mixtral rule (softmax, top-k,
+ * renormalised).
+ *
+ * Conventions for every call
+ * --------------------------
+ *  - Every pointer argument is a DEVICE pointer owned by the caller, except
+ *    the config pointer and the debug-struct pointer (host memory). The library
+ *    never allocates or frees device memory; scratch space is the caller's
+ *    workspace `ws` of at least moe_workspace_size() bytes, passed with its
+ *    size `ws_bytes`.
+ *  - Calls validate their arguments synchronously, then enqueue kernels on the
+ *    given stream(s) and return without synchronising. A non-zero return
+ *    means nothing was enqueued (validation) or a launch failed (MOE_ERR_HIP);
+ *    moe_last_error() then holds a message (per calling thread).
+ *  - T = 0 is a valid no-op. No C++ exception crosses this interface.
+ *  - Layouts are row-major and dense:
+ *      x          [T][d]          activations, dtype
+ *      w_router   [E][d]          router weight, one row per expert, dtype
+ *      bias       [E]             fp32 selection bias (sigmoid routing only)
+ *      w_gate     [E][I][d]       expert gate projections (GEMM1, gate half)
+ *      w_up       [E][I][d]       expert up projections   (GEMM1, up half)
+ *      w_down     [E][d][I]       expert down projections (GEMM2)
+ *      ws_gate, ws_up [I_shared][d], ws_down [d][I_shared]  shared expert
+ *    Every weight matrix is stored output-feature-major, so its reduction
+ *    dimension is contiguous.
+ *  - dtype MOE_BF16: activations and weights bf16, every product accumulated
+ *    in fp32, the SwiGLU output and the expert outputs rounded to bf16 (round
+ *    to nearest even). dtype MOE_F32: fp32 throughout.
+ *  - Supported: 1 <= E <= 256, 1 <= k <= min(E, 16), d and I multiples of 64,
+ *    n_shared in {0, 1}; larger or other shapes return MOE_ERR_UNSUPPORTED.
+ *    Inputs must be finite.
+ *  - Results are deterministic: two calls on the same inputs give the same
+ *    bits, whatever the stream arrangement (no atomics decide any order).
+ *  - Calls that share one workspace must not overlap in time.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1, /* NULL required pointer, T < 0, inconsistent config */
+  MOE_ERR_UNSUPPORTED = -2, /* valid but outside the supported shapes/dtypes  */
+  MOE_ERR_WORKSPACE = -3,   /* ws_bytes smaller than moe_workspace_size()     */
+  MOE_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed     */
+} moe_status_t;
+
+typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype_t;
+
+typedef enum {
+  MOE_SCORE_SOFTMAX = 0, /* Mixtral: softmax scores, selection on the logit     */
+  MOE_SCORE_SIGMOID = 1  /* DeepSeek-V3: sigmoid scores, selection on s + bias  */
+} moe_score_t;
+
+typedef struct {
+  int32_t d;           /* hidden size                                         */
+  int32_t E;           /* routed experts                                      */
+  int32_t k;           /* experts selected per token                          */
+  int32_t n_groups;    /* expert groups for the group limit (1 = no limit)    */
+  int32_t topk_groups; /* groups kept per token                               */
+  int32_t I;           /* routed-expert intermediate size                     */
+  int32_t n_shared;    /* shared experts, 0 or 1                              */
+  int32_t I_shared;    /* shared-expert intermediate size                     */
+  int32_t score;       /* moe_score_t                                         */
+  int32_t renorm;      /* 1: divide the selected scores by their sum          */
+  float route_scale;   /* multiplies every weight (1.0 Mixtral, 2.5 DSV3)     */
+  int32_t dtype;       /* moe_dtype_t                                         */
+} moe_config_t;
+
+/* Optional device buffers moe_layer writes its intermediates into (each may be
+ * NULL; a NULL entry keeps that intermediate in the workspace). Sizes as in
+ * moe_route/moe_dispatch/moe_expert_ffn/moe_shared_ffn. */
+typedef struct {
+  float* logits;          /* [T][E]   */
+  int32_t* topk_idx;      /* [T][k]   */
+  float* topk_w;          /* [T][k]   */
+  int32_t* counts;        /* [E]      */
+  int32_t* offsets;       /* [E+1]    */
+  int32_t* sorted_token;  /* [T*k]    */
+  int32_t* sorted_assign; /* [T*k]    */
+  int32_t* inv_perm;      /* [T*k]    */
+  void* y_perm;           /* [T*k][d] dtype */
+  void* shared_out;       /* [T][d]   dtype (n_shared = 1 only) */
+} moe_layer_debug_t;
+
+/* Bytes of workspace any call below needs for this config and token count
+ * (the maximum over the calls; 0 if the config is invalid). */
+size_t moe_workspace_size(const moe_config_t* cfg, int32_t T);
+
+/*
+ * moe_route — gating and top-k routing (App. M: each token is routed to its
+ * experts before the dispatch; selection rule as in the header comment).
+ *  x, w_router : if x != NULL, logits = x · w_routerᵀ is computed (fp32
+ *                accumulation) and written to `logits`; if x == NULL,
+ *                `logits` is an input and w_router is ignored.
+ *  bias        : [E] fp32 added to the sigmoid scores for selection only;
+ *                may be NULL (no bias); must be NULL for softmax routing.
+ *  logits      : [T][E] fp32, required.
+ *  topk_idx    : [T][k] int32 out, each row ordered by key descending, lower
+ *                expert index first on ties.
+ *  topk_w      : [T][k] fp32 out: selected scores (softmax probabilities or
+ *                unbiased sigmoid), divided by their sum if cfg->renorm, times
+ *                cfg->route_scale.
+ * Keys, group scores and weights are evaluated in fp64 from the fp32 logits,
+ * so the selection is a deterministic function of the logits' bits.
+ */
+int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_router,
+              const float* bias, float* logits, int32_t* topk_idx, float* topk_w,
+              hipStream_t stream);
+
+/*
+ * moe_dispatch — the single-GPU form of the dispatch all-to-all (App. F,
+ * first exchange of the host pipeline; App. M: variable-size, unpadded
+ * per-destination transfers). Assignment a = t*k + j sends token t to expert
+ * topk_idx[t][j]; rows are grouped by expert, tokens ascending inside a group.
+ *  counts        : [E] out, assignments per expert.
+ *  offsets       : [E+1] out, exclusive prefix sum of counts (offsets[E] = T*k).
+ *  sorted_token  : [T*k] out, token of every dispatched row.
+ *  sorted_assign : [T*k] out or NULL, assignment of every row.
+ *  inv_perm      : [T*k] out, row of every assignment.
+ *  ws            : workspace (per-chunk expert masks and bases).
+ */
+int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, int32_t* counts,
+                 int32_t* offsets, int32_t* sorted_token, int32_t* sorted_assign,
+                 int32_t* inv_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_expert_ffn — the per-expert SwiGLU FFN over the dispatched rows
+ * (App. M step 3 / App. F: GEMM1 gate+up, SwiGLU, GEMM2 down), as one grouped
+ * GEMM pair: for every expert e and row r in [offsets[e], offsets[e+1]):
+ *   h[r]      = silu(x[sorted_token[r]] · w_gate[e]ᵀ) * (x[sorted_token[r]] · w_up[e]ᵀ)
+ *   y_perm[r] = h[r] · w_down[e]ᵀ
+ * The row gather is fused into the GEMM's operand load. h lives in the
+ * workspace (dtype, [T*k][I]).
+ *  y_perm : [T*k][d] dtype out.
+ */
+int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x,
+                   const int32_t* sorted_token, const int32_t* offsets, const void* w_gate,
+                   const void* w_up, const void* w_down, void* y_perm, void* ws,
+                   size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_shared_ffn — the shared expert: the same SwiGLU FFN, with intermediate
+ * size cfg->I_shared, applied to all T tokens (dense, unweighted).
+ *  out : [T][d] dtype out. Requires cfg->n_shared == 1.
+ */
+int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void* ws_gate,
+                   const void* ws_up, const void* ws_down, void* out, void* ws,
+                   size_t ws_bytes, hipStream_t stream);
+
+/*
+ * moe_combine — the single-GPU form of the combine all-to-all (App. F, second
+ * exchange): a weighted gather back to token order,
+ *   out[t] = sum_{j=0..k-1} topk_w[t][j] * y_perm[inv_perm[t*k+j]]  (+ shared_out[t])
+ * with the slots summed in ascending j in fp32 and the shared expert added with
+ * weight 1 when shared_out != NULL. No atomics: each output row is produced
+ * by one workgroup.
+ *  out : [T][d] dtype out.
+ */
+int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const int32_t* inv_perm,
+                const float* topk_w, const void* shared_out, void* out, hipStream_t stream);
+
+/*
+ * moe_layer — the whole layer: route, dispatch, expert FFN and combine on
+ * s_main; the shared expert on s_aux, overlapping the routing and dispatch
+ * (the single-GPU form of the paper's two-stream overlap, §4.3: dispatch on
+ * one stream concurrent with expert compute on another, joined by an event).
+ *  s_aux  : may be NULL or equal to s_main (then everything runs on s_main).
+ *  ws_*   : shared-expert weights, required iff cfg->n_shared == 1.
+ *  out    : [T][d] dtype out.
+ *  dbg    : NULL, or device buffers to receive intermediates (see above).
+ * On return, s_main carries all the work (s_aux is joined into it).
+ */
+int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_router,
+              const float* bias, const void* w_gate, const void* w_up, const void* w_down,
+              const void* ws_gate, const void* ws_up, const void* ws_down, void* out, void* ws,
+              size_t ws_bytes, hipStream_t s_main, hipStream_t s_aux, moe_layer_debug_t* dbg);
+
+/* Static text for a moe_status_t. */
+const char* moe_status_string(int status);
+/* Message of the last failing call on this thread ("" if none). */
+const char* moe_last_error(void);
+/* Library version string. */
+const char* moe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

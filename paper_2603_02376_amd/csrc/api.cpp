@@ -1,0 +1,447 @@
+// C ABI of the MoE-layer library: argument validation, workspace layout and
+// the orchestration of the kernels (route, dispatch, expert FFN, shared
+// expert, combine). Every step of the layer runs in the library's own HIP
+// kernels; this file only checks arguments and enqueues launches.
+#include "moe.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <mutex>
+#include <string>
+
+#include "moe_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(MOE_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+size_t esize(const moe_config_t& c) { return c.dtype == MOE_BF16 ? 2 : 4; }
+
+// Byte offsets of every scratch region inside the caller's workspace.
+struct Layout {
+  size_t logits, topk_idx, topk_w, masks, bases, counts, offsets, sorted_token, sorted_assign,
+      inv_perm, h, y_perm, shared_h, shared_out, total;
+};
+
+Layout make_layout(const moe_config_t& c, int32_t T) {
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t t = (size_t)T, tk = (size_t)T * c.k, es = esize(c);
+  const size_t nch = (t + moe::kDispatchChunk - 1) / moe::kDispatchChunk;
+  L.logits = take(t * c.E * 4);
+  L.topk_idx = take(tk * 4);
+  L.topk_w = take(tk * 4);
+  L.masks = take(nch * c.E * 8);
+  L.bases = take(nch * c.E * 4);
+  L.counts = take((size_t)c.E * 4);
+  L.offsets = take((size_t)(c.E + 1) * 4);
+  L.sorted_token = take(tk * 4);
+  L.sorted_assign = take(tk * 4);
+  L.inv_perm = take(tk * 4);
+  L.h = take(tk * c.I * es);
+  L.y_perm = take(tk * c.d * es);
+  L.shared_h = take(c.n_shared ? t * c.I_shared * es : 0);
+  L.shared_out = take(c.n_shared ? t * c.d * es : 0);
+  L.total = off;
+  return L;
+}
+
+int validate(const moe_config_t* c, int32_t T) {
+  if (!c) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
+  if (T < 0) return fail(MOE_ERR_INVALID_ARG, "T < 0");
+  if (c->d <= 0 || c->E <= 0 || c->k <= 0 || c->I <= 0)
+    return fail(MOE_ERR_INVALID_ARG, "d, E, k and I must be positive");
+  if (c->k > c->E) return fail(MOE_ERR_INVALID_ARG, "k > E");
+  if (c->n_groups < 1 || c->E % c->n_groups != 0)
+    return fail(MOE_ERR_INVALID_ARG, "E must be a positive multiple of n_groups");
+  if (c->topk_groups < 1 || c->topk_groups > c->n_groups)
+    return fail(MOE_ERR_INVALID_ARG, "need 1 <= topk_groups <= n_groups");
+  if (c->n_groups > 1 && (int64_t)c->k > (int64_t)c->topk_groups * (c->E / c->n_groups))
+    return fail(MOE_ERR_INVALID_ARG, "k exceeds the experts left by the group limit");
+  if (c->score != MOE_SCORE_SOFTMAX && c->score != MOE_SCORE_SIGMOID)
+    return fail(MOE_ERR_INVALID_ARG, "unknown score function");
+  if (c->n_shared < 0) return fail(MOE_ERR_INVALID_ARG, "n_shared < 0");
+  if (c->n_shared > 0 && c->I_shared <= 0) return fail(MOE_ERR_INVALID_ARG, "I_shared must be positive");
+  if (!std::isfinite(c->route_scale)) return fail(MOE_ERR_INVALID_ARG, "route_scale is not finite");
+  if (c->dtype != MOE_F32 && c->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "unknown dtype");
+  if (c->E > 256) return fail(MOE_ERR_UNSUPPORTED, "E > 256");
+  if (c->k > 16) return fail(MOE_ERR_UNSUPPORTED, "k > 16");
+  if (c->n_groups > 64) return fail(MOE_ERR_UNSUPPORTED, "n_groups > 64");
+  if (c->n_shared > 1) return fail(MOE_ERR_UNSUPPORTED, "n_shared > 1");
+  if (c->d % 64 != 0 || c->I % 64 != 0 || (c->n_shared && c->I_shared % 64 != 0))
+    return fail(MOE_ERR_UNSUPPORTED, "d, I and I_shared must be multiples of 64");
+  if ((int64_t)T * c->k >= (int64_t)1 << 31) return fail(MOE_ERR_UNSUPPORTED, "T*k >= 2^31");
+  return MOE_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int need(const void* p, const char* name) {
+  if (!p) return fail(MOE_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  if (!aligned16(p)) return fail(MOE_ERR_INVALID_ARG, std::string(name) + " is not 16-byte aligned");
+  return MOE_OK;
+}
+
+#define MOE_CHECK(expr)            \
+  do {                             \
+    const int _s = (expr);         \
+    if (_s != MOE_OK) return _s;   \
+  } while (0)
+
+int check_ws(const moe_config_t* c, int32_t T, void* ws, size_t ws_bytes) {
+  if (!ws) return fail(MOE_ERR_INVALID_ARG, "ws is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(MOE_ERR_INVALID_ARG, "ws is not 256-byte aligned");
+  const size_t want = make_layout(*c, T).total;
+  if (ws_bytes < want)
+    return fail(MOE_ERR_WORKSPACE, "workspace too small: need " + std::to_string(want) + " bytes, got " +
+                                       std::to_string(ws_bytes));
+  return MOE_OK;
+}
+
+// ---- internal launch helpers (arguments already validated) -----------------
+
+hipError_t run_gemm(const moe_config_t& c, const moe::GemmProblem& p, int epi, bool out_f32, hipStream_t s) {
+  if (c.dtype == MOE_BF16) return moe::launch_gemm_bf16(p, epi, out_f32, s);
+  return moe::launch_gemm_f32(p, epi, s);
+}
+
+hipError_t run_gate(const moe_config_t& c, int32_t T, const void* x, const void* w_router, float* logits,
+                    hipStream_t s) {
+  moe::GemmProblem g{};
+  g.A = x;
+  g.a_rows = T;
+  g.groups = 1;
+  g.M = T;
+  g.B0 = w_router;
+  g.N = c.E;
+  g.K = c.d;
+  g.C = logits;
+  g.ldc = c.E;
+  return run_gemm(c, g, moe::EPI_STORE, true, s);
+}
+
+hipError_t run_route(const moe_config_t& c, int32_t T, const float* bias, const float* logits, int32_t* idx,
+                     float* w, hipStream_t s) {
+  moe::RouteParams r{};
+  r.logits = logits;
+  r.bias = (c.score == MOE_SCORE_SIGMOID) ? bias : nullptr;
+  r.T = T;
+  r.E = c.E;
+  r.k = c.k;
+  r.n_groups = c.n_groups;
+  r.topk_groups = c.topk_groups;
+  r.score = c.score;
+  r.renorm = c.renorm;
+  r.scale = c.route_scale;
+  r.topk_idx = idx;
+  r.topk_w = w;
+  return moe::launch_route(r, s);
+}
+
+hipError_t run_dispatch(const moe_config_t& c, int32_t T, const int32_t* idx, char* ws, const Layout& L,
+                        int32_t* counts, int32_t* offsets, int32_t* st, int32_t* sa, int32_t* inv, hipStream_t s) {
+  moe::DispatchParams d{};
+  d.topk_idx = idx;
+  d.T = T;
+  d.E = c.E;
+  d.k = c.k;
+  d.masks = reinterpret_cast<uint64_t*>(ws + L.masks);
+  d.bases = reinterpret_cast<int32_t*>(ws + L.bases);
+  d.counts = counts;
+  d.offsets = offsets;
+  d.sorted_token = st;
+  d.sorted_assign = sa;
+  d.inv_perm = inv;
+  return moe::launch_dispatch(d, s);
+}
+
+// Dense or grouped SwiGLU FFN: h = silu(X Wgᵀ) * (X Wuᵀ) into `h`, then
+// y = h Wdᵀ into `y`.
+hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
+                   const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
+                   void* h, void* y, hipStream_t s) {
+  moe::GemmProblem up{};
+  up.A = x;
+  up.a_rows = a_rows;
+  up.gather = gather;
+  up.offsets = offsets;
+  up.groups = groups;
+  up.M = rows;
+  up.B0 = wg;
+  up.B1 = wu;
+  up.N = inter;
+  up.K = c.d;
+  up.C = h;
+  up.ldc = inter;
+  hipError_t e = run_gemm(c, up, moe::EPI_SWIGLU, false, s);
+  if (e != hipSuccess) return e;
+  moe::GemmProblem down{};
+  down.A = h;
+  down.a_rows = rows;
+  down.offsets = offsets;
+  down.groups = groups;
+  down.M = rows;
+  down.B0 = wd;
+  down.N = c.d;
+  down.K = inter;
+  down.C = y;
+  down.ldc = c.d;
+  return run_gemm(c, down, moe::EPI_STORE, false, s);
+}
+
+hipError_t run_combine(const moe_config_t& c, int32_t T, const void* y, const int32_t* inv, const float* w,
+                       const void* shared, void* out, hipStream_t s) {
+  moe::CombineParams p{};
+  p.y_perm = y;
+  p.inv_perm = inv;
+  p.topk_w = w;
+  p.shared_out = shared;
+  p.out = out;
+  p.T = T;
+  p.k = c.k;
+  p.d = c.d;
+  return moe::launch_combine(p, c.dtype == MOE_BF16, s);
+}
+
+// Two events per (thread, device) for the fork/join of moe_layer's streams.
+struct StreamEvents {
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+
+hipError_t layer_events(StreamEvents** out) {
+  thread_local StreamEvents ev[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  StreamEvents& se = ev[dev];
+  if (!se.fork) {
+    e = hipEventCreateWithFlags(&se.fork, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+    e = hipEventCreateWithFlags(&se.join, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+  }
+  *out = &se;
+  return hipSuccess;
+}
+
+}  // namespace
+
+namespace moe {
+
+int device_cu_count() {
+  static std::mutex mu;
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+}  // namespace moe
+
+extern "C" {
+
+size_t moe_workspace_size(const moe_config_t* cfg, int32_t T) {
+  const std::string saved = g_last_error;
+  if (validate(cfg, T) != MOE_OK) return 0;
+  g_last_error = saved;
+  return make_layout(*cfg, T).total;
+}
+
+int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_router, const float* bias,
+              float* logits, int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  if (cfg->score == MOE_SCORE_SOFTMAX && bias) return fail(MOE_ERR_INVALID_ARG, "bias given for softmax routing");
+  MOE_CHECK(need(logits, "logits"));
+  MOE_CHECK(need(topk_idx, "topk_idx"));
+  MOE_CHECK(need(topk_w, "topk_w"));
+  if (x) {
+    MOE_CHECK(need(x, "x"));
+    MOE_CHECK(need(w_router, "w_router"));
+  }
+  if (T == 0) return MOE_OK;
+  hipError_t e;
+  if (x && (e = run_gate(*cfg, T, x, w_router, logits, stream)) != hipSuccess) return hip_fail(e, "gate GEMM");
+  if ((e = run_route(*cfg, T, bias, logits, topk_idx, topk_w, stream)) != hipSuccess) return hip_fail(e, "route");
+  return MOE_OK;
+}
+
+int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, int32_t* counts, int32_t* offsets,
+                 int32_t* sorted_token, int32_t* sorted_assign, int32_t* inv_perm, void* ws, size_t ws_bytes,
+                 hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  MOE_CHECK(need(topk_idx, "topk_idx"));
+  MOE_CHECK(need(counts, "counts"));
+  MOE_CHECK(need(offsets, "offsets"));
+  MOE_CHECK(need(sorted_token, "sorted_token"));
+  MOE_CHECK(need(inv_perm, "inv_perm"));
+  if (sorted_assign && !aligned16(sorted_assign)) return fail(MOE_ERR_INVALID_ARG, "sorted_assign is not 16-byte aligned");
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  if (T == 0) return MOE_OK;
+  const Layout L = make_layout(*cfg, T);
+  const hipError_t e = run_dispatch(*cfg, T, topk_idx, static_cast<char*>(ws), L, counts, offsets, sorted_token,
+                                    sorted_assign, inv_perm, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "dispatch");
+}
+
+int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int32_t* sorted_token,
+                   const int32_t* offsets, const void* w_gate, const void* w_up, const void* w_down, void* y_perm,
+                   void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  MOE_CHECK(need(x, "x"));
+  MOE_CHECK(need(sorted_token, "sorted_token"));
+  MOE_CHECK(need(offsets, "offsets"));
+  MOE_CHECK(need(w_gate, "w_gate"));
+  MOE_CHECK(need(w_up, "w_up"));
+  MOE_CHECK(need(w_down, "w_down"));
+  MOE_CHECK(need(y_perm, "y_perm"));
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  if (T == 0) return MOE_OK;
+  const Layout L = make_layout(*cfg, T);
+  const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
+                               static_cast<char*>(ws) + L.h, y_perm, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
+}
+
+int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void* ws_gate, const void* ws_up,
+                   const void* ws_down, void* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  if (cfg->n_shared != 1) return fail(MOE_ERR_INVALID_ARG, "config has no shared expert");
+  MOE_CHECK(need(x, "x"));
+  MOE_CHECK(need(ws_gate, "ws_gate"));
+  MOE_CHECK(need(ws_up, "ws_up"));
+  MOE_CHECK(need(ws_down, "ws_down"));
+  MOE_CHECK(need(out, "out"));
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  if (T == 0) return MOE_OK;
+  const Layout L = make_layout(*cfg, T);
+  const hipError_t e = run_ffn(*cfg, T, T, 1, cfg->I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down,
+                               static_cast<char*>(ws) + L.shared_h, out, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "shared FFN");
+}
+
+int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const int32_t* inv_perm,
+                const float* topk_w, const void* shared_out, void* out, hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  MOE_CHECK(need(y_perm, "y_perm"));
+  MOE_CHECK(need(inv_perm, "inv_perm"));
+  MOE_CHECK(need(topk_w, "topk_w"));
+  MOE_CHECK(need(out, "out"));
+  if (shared_out && !aligned16(shared_out)) return fail(MOE_ERR_INVALID_ARG, "shared_out is not 16-byte aligned");
+  if (T == 0) return MOE_OK;
+  const hipError_t e = run_combine(*cfg, T, y_perm, inv_perm, topk_w, shared_out, out, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "combine");
+}
+
+int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_router, const float* bias,
+              const void* w_gate, const void* w_up, const void* w_down, const void* ws_gate, const void* ws_up,
+              const void* ws_down, void* out, void* ws, size_t ws_bytes, hipStream_t s_main, hipStream_t s_aux,
+              moe_layer_debug_t* dbg) {
+  MOE_CHECK(validate(cfg, T));
+  const moe_config_t& c = *cfg;
+  if (c.score == MOE_SCORE_SOFTMAX && bias) return fail(MOE_ERR_INVALID_ARG, "bias given for softmax routing");
+  MOE_CHECK(need(x, "x"));
+  MOE_CHECK(need(w_router, "w_router"));
+  MOE_CHECK(need(w_gate, "w_gate"));
+  MOE_CHECK(need(w_up, "w_up"));
+  MOE_CHECK(need(w_down, "w_down"));
+  MOE_CHECK(need(out, "out"));
+  if (c.n_shared) {
+    MOE_CHECK(need(ws_gate, "ws_gate"));
+    MOE_CHECK(need(ws_up, "ws_up"));
+    MOE_CHECK(need(ws_down, "ws_down"));
+  }
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  moe_layer_debug_t none{};
+  const moe_layer_debug_t& d = dbg ? *dbg : none;
+  const void* dptrs[] = {d.logits, d.topk_idx, d.topk_w, d.counts, d.offsets, d.sorted_token,
+                         d.sorted_assign, d.inv_perm, d.y_perm, d.shared_out};
+  for (const void* p : dptrs)
+    if (p && !aligned16(p)) return fail(MOE_ERR_INVALID_ARG, "debug buffer is not 16-byte aligned");
+  if (d.shared_out && !c.n_shared) return fail(MOE_ERR_INVALID_ARG, "debug shared_out without a shared expert");
+  if (T == 0) return MOE_OK;
+
+  const Layout L = make_layout(c, T);
+  char* w = static_cast<char*>(ws);
+  float* logits = d.logits ? d.logits : reinterpret_cast<float*>(w + L.logits);
+  int32_t* idx = d.topk_idx ? d.topk_idx : reinterpret_cast<int32_t*>(w + L.topk_idx);
+  float* tw = d.topk_w ? d.topk_w : reinterpret_cast<float*>(w + L.topk_w);
+  int32_t* counts = d.counts ? d.counts : reinterpret_cast<int32_t*>(w + L.counts);
+  int32_t* offsets = d.offsets ? d.offsets : reinterpret_cast<int32_t*>(w + L.offsets);
+  int32_t* st = d.sorted_token ? d.sorted_token : reinterpret_cast<int32_t*>(w + L.sorted_token);
+  int32_t* inv = d.inv_perm ? d.inv_perm : reinterpret_cast<int32_t*>(w + L.inv_perm);
+  void* y = d.y_perm ? d.y_perm : w + L.y_perm;
+  void* shared = c.n_shared ? (d.shared_out ? d.shared_out : w + L.shared_out) : nullptr;
+
+  hipError_t e;
+  const bool two = c.n_shared && s_aux && s_aux != s_main;
+  StreamEvents* ev = nullptr;
+  if (two) {
+    // fork: the shared expert on s_aux may start once x is ready on s_main
+    if ((e = layer_events(&ev)) != hipSuccess) return hip_fail(e, "event create");
+    if ((e = hipEventRecord(ev->fork, s_main)) != hipSuccess) return hip_fail(e, "event record");
+    if ((e = hipStreamWaitEvent(s_aux, ev->fork, 0)) != hipSuccess) return hip_fail(e, "stream wait");
+    if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h, shared,
+                     s_aux)) != hipSuccess)
+      return hip_fail(e, "shared FFN");
+    if ((e = hipEventRecord(ev->join, s_aux)) != hipSuccess) return hip_fail(e, "event record");
+  }
+  if ((e = run_gate(c, T, x, w_router, logits, s_main)) != hipSuccess) return hip_fail(e, "gate GEMM");
+  if ((e = run_route(c, T, bias, logits, idx, tw, s_main)) != hipSuccess) return hip_fail(e, "route");
+  if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main)) != hipSuccess)
+    return hip_fail(e, "dispatch");
+  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main)) != hipSuccess)
+    return hip_fail(e, "expert FFN");
+  if (c.n_shared) {
+    if (two) {
+      if ((e = hipStreamWaitEvent(s_main, ev->join, 0)) != hipSuccess) return hip_fail(e, "stream wait");
+    } else if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h,
+                            shared, s_main)) != hipSuccess) {
+      return hip_fail(e, "shared FFN");
+    }
+  }
+  if ((e = run_combine(c, T, y, inv, tw, shared, out, s_main)) != hipSuccess) return hip_fail(e, "combine");
+  return MOE_OK;
+}
+
+const char* moe_status_string(int status) {
+  switch (status) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported configuration";
+    case MOE_ERR_WORKSPACE: return "workspace too small";
+    case MOE_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* moe_last_error(void) { return g_last_error.c_str(); }
+
+const char* moe_version(void) { return "moe-mi355x 0.1.0 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+// Combine: the single-GPU form of the paper's combine all-to-all (App. F,
+// second exchange), out[t] = sum_j w[t][j] * y_perm[inv_perm[t*k+j]] (+ shared[t]).
+//
+// Atomic-free: one workgroup owns one output row and gathers its k expert
+// rows through the inverse permutation, so the sum order (j ascending, then
+// the shared expert) is fixed and the result is bit-reproducible. The kernel
+// is HBM-bound (k+1 rows read, one written per token); every thread moves 8
+// elements per access (16 bytes for bf16) and keeps the k row indices and
+// weights in registers.
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int kThreads = 128;
+constexpr int kMaxK = 16;
+
+struct Vec8 {
+  float v[8];
+};
+
+__device__ __forceinline__ Vec8 load8(const __bf16* p) {
+  const i32x4 raw = *reinterpret_cast<const i32x4*>(p);
+  const bf16x8 h = __builtin_bit_cast(bf16x8, raw);
+  Vec8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r.v[i] = static_cast<float>(h[i]);
+  return r;
+}
+__device__ __forceinline__ Vec8 load8(const float* p) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p);
+  const f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+  Vec8 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r.v[i] = a[i];
+    r.v[i + 4] = b[i];
+  }
+  return r;
+}
+__device__ __forceinline__ void store8(__bf16* p, const Vec8& x) {
+  bf16x8 h;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) h[i] = static_cast<__bf16>(x.v[i]);
+  *reinterpret_cast<i32x4*>(p) = __builtin_bit_cast(i32x4, h);
+}
+__device__ __forceinline__ void store8(float* p, const Vec8& x) {
+  f32x4 a, b;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a[i] = x.v[i];
+    b[i] = x.v[i + 4];
+  }
+  *reinterpret_cast<f32x4*>(p) = a;
+  *reinterpret_cast<f32x4*>(p + 4) = b;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
+  const int t = blockIdx.x;
+  const int k = p.k;
+  const size_t d = (size_t)p.d;
+  const T* Y = static_cast<const T*>(p.y_perm);
+  const T* S = static_cast<const T*>(p.shared_out);
+  T* O = static_cast<T*>(p.out);
+  int rows[kMaxK];
+  float w[kMaxK];
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j < k) {
+      rows[j] = min(max(p.inv_perm[(size_t)t * k + j], 0), p.T * k - 1);
+      w[j] = p.topk_w[(size_t)t * k + j];
+    }
+  }
+  for (int c = threadIdx.x * 8; c < p.d; c += kThreads * 8) {
+    Vec8 acc;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc.v[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (j < k) {
+        const Vec8 y = load8(Y + (size_t)rows[j] * d + c);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc.v[i] = fmaf(w[j], y.v[i], acc.v[i]);
+      }
+    }
+    if (S) {
+      const Vec8 s = load8(S + (size_t)t * d + c);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc.v[i] += s.v[i];
+    }
+    store8(O + (size_t)t * d + c, acc);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(const CombineParams& p, bool bf16, hipStream_t s) {
+  if (p.T <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(combine_kernel<__bf16>, dim3(p.T), dim3(kThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(combine_kernel<float>, dim3(p.T), dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace moe

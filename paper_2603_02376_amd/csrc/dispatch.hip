@@ -1,0 +1,132 @@
+// Dispatch: the single-GPU form of the paper's dispatch all-to-all (App. F,
+// first exchange; App. M, variable-size unpadded per-destination transfers).
+//
+// The T*k assignments (t, j) -> expert topk_idx[t][j] are grouped by expert,
+// tokens ascending inside every group: a stable counting sort. Stability is
+// what makes the permutation a well-defined, bit-reproducible result, so no
+// atomic may decide the order of rows. Three small kernels:
+//
+//   1. count   — one wavefront per chunk of 64 tokens; lane = token. Every lane
+//                ORs its bit into an LDS bitmask per expert it selected (a
+//                token holds at most one slot per expert). The masks are
+//                written out per (chunk, expert). OR is order-independent, so
+//                the masks are deterministic.
+//   2. scan    — one workgroup: per expert, the exclusive prefix of popcounts
+//                over chunks (the chunk's base inside the expert's segment),
+//                the per-expert count, and the exclusive prefix over experts
+//                (offsets).
+//   3. scatter — same grid as 1: the row of (t, j) is
+//                offsets[e] + base[chunk][e] + popcount(mask[chunk][e] & lanes below t),
+//                i.e. the number of earlier tokens that chose e.
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int kWaves = 4;  // chunks per workgroup
+
+__global__ void __launch_bounds__(64 * kWaves) dispatch_count_kernel(DispatchParams p) {
+  __shared__ unsigned long long m[kWaves][256];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;
+  const int chunk = blockIdx.x * kWaves + wave;
+  const int t = chunk * kDispatchChunk + lane;
+  for (int e = lane; e < p.E; e += 64) m[wave][e] = 0ull;
+  __syncthreads();
+  if (chunk < nchunks && t < p.T) {
+    for (int j = 0; j < p.k; ++j) {
+      const int e = p.topk_idx[(size_t)t * p.k + j];
+      if ((unsigned)e < (unsigned)p.E) atomicOr(&m[wave][e], 1ull << lane);
+    }
+  }
+  __syncthreads();
+  if (chunk < nchunks)
+    for (int e = lane; e < p.E; e += 64) p.masks[(size_t)chunk * p.E + e] = m[wave][e];
+}
+
+// One workgroup of 1024 threads: thread (part, e) with part in [0, 4) scans a
+// quarter of the chunks for expert e; the four partial sums are combined
+// through LDS.
+__global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
+  __shared__ int part_sum[4][256];
+  __shared__ int wsum[16];
+  const int e = threadIdx.x & 255;
+  const int part = threadIdx.x >> 8;
+  const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;
+  const int per = (nchunks + 3) / 4;
+  const int c0 = part * per, c1 = min(nchunks, c0 + per);
+  int run = 0;
+  if (e < p.E) {
+    for (int c = c0; c < c1; ++c) run += __popcll(p.masks[(size_t)c * p.E + e]);
+  }
+  part_sum[part][e] = run;
+  __syncthreads();
+  int base = 0, cnt = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int v = part_sum[q][e];
+    if (q < part) base += v;
+    cnt += v;
+  }
+  if (e < p.E) {
+    for (int c = c0; c < c1; ++c) {
+      const size_t i = (size_t)c * p.E + e;
+      p.bases[i] = base;
+      base += __popcll(p.masks[i]);
+    }
+  }
+  // exclusive scan of the counts over experts (threads of part 0)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int v = (part == 0 && e < p.E) ? cnt : 0;
+  int inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int n = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += n;
+  }
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  if (part == 0) {
+    int off = 0, tot = 0;
+    for (int w = 0; w < 4; ++w) {
+      if (w < wave) off += wsum[w];
+      tot += wsum[w];
+    }
+    if (e < p.E) {
+      p.counts[e] = cnt;
+      p.offsets[e] = off + inc - v;
+    }
+    if (e == 0) p.offsets[p.E] = tot;
+  }
+}
+
+__global__ void __launch_bounds__(64 * kWaves) dispatch_scatter_kernel(DispatchParams p) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int chunk = blockIdx.x * kWaves + wave;
+  const int t = chunk * kDispatchChunk + lane;
+  if (t >= p.T) return;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int j = 0; j < p.k; ++j) {
+    const int a = t * p.k + j;
+    const int e = p.topk_idx[a];
+    if ((unsigned)e >= (unsigned)p.E) continue;  // invalid input: row left unassigned
+    const size_t ci = (size_t)chunk * p.E + e;
+    const int row = p.offsets[e] + p.bases[ci] + __popcll(p.masks[ci] & below);
+    p.sorted_token[row] = t;
+    if (p.sorted_assign) p.sorted_assign[row] = a;
+    p.inv_perm[a] = row;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dispatch(const DispatchParams& p, hipStream_t s) {
+  const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;
+  const int blocks = (nchunks + kWaves - 1) / kWaves;
+  if (blocks > 0) hipLaunchKernelGGL(dispatch_count_kernel, dim3(blocks), dim3(64 * kWaves), 0, s, p);
+  hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(1024), 0, s, p);
+  if (blocks > 0) hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(blocks), dim3(64 * kWaves), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace moe

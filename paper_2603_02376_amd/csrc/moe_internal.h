@@ -1,0 +1,91 @@
+// Internal declarations shared by the kernel sources and the C-ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Epilogue of the grouped GEMM.
+enum GemmEpilogue : int {
+  EPI_STORE = 0,   // C = A·Bᵀ
+  EPI_SWIGLU = 1,  // C = silu(A·B0ᵀ) * (A·B1ᵀ)
+};
+
+// One grouped GEMM "C[r] = op(A[gather[r]] · B_g)" over row segments.
+//   A       : [*][K] row-major; row r of the problem reads A row gather[r]
+//             (gather == nullptr: A row r).
+//   offsets : [groups+1] device array; group g owns rows [offsets[g], offsets[g+1]).
+//             nullptr: a single group of M rows.
+//   B0, B1  : [groups][N][K] row-major (B1 only for EPI_SWIGLU).
+//   C       : [M][ldc], N columns written per row.
+// Malformed offsets or gather indices are clamped into range: they give
+// unspecified results but never an out-of-bounds access.
+struct GemmProblem {
+  const void* A;
+  int32_t a_rows;  // rows of A; gathered indices are clamped into [0, a_rows)
+  const int32_t* gather;
+  const int32_t* offsets;
+  int32_t groups;
+  int32_t M;  // upper bound on the rows (exact when offsets == nullptr)
+  const void* B0;
+  const void* B1;
+  int32_t N;
+  int32_t K;
+  void* C;
+  int32_t ldc;
+};
+
+// bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
+// only); otherwise outputs are bf16.
+hipError_t launch_gemm_bf16(const GemmProblem& p, int epilogue, bool out_f32, hipStream_t s);
+// fp32 grouped GEMM (vector ALU), same semantics, fp32 in and out.
+hipError_t launch_gemm_f32(const GemmProblem& p, int epilogue, hipStream_t s);
+
+struct RouteParams {
+  const float* logits;  // [T][E]
+  const float* bias;    // [E] or nullptr
+  int32_t T, E, k, n_groups, topk_groups, score, renorm;
+  float scale;
+  int32_t* topk_idx;  // [T][k]
+  float* topk_w;      // [T][k]
+};
+hipError_t launch_route(const RouteParams& p, hipStream_t s);
+
+// Dispatch scratch: per 64-token chunk, an expert bitmask of the chunk's
+// tokens ([chunks][E] uint64) and the rank base of the chunk inside every
+// expert's segment ([chunks][E] int32).
+constexpr int kDispatchChunk = 64;
+struct DispatchParams {
+  const int32_t* topk_idx;
+  int32_t T, E, k;
+  uint64_t* masks;
+  int32_t* bases;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* sorted_token;
+  int32_t* sorted_assign;  // may be nullptr
+  int32_t* inv_perm;
+};
+hipError_t launch_dispatch(const DispatchParams& p, hipStream_t s);
+
+struct CombineParams {
+  const void* y_perm;      // [T*k][d]
+  const int32_t* inv_perm; // [T*k]
+  const float* topk_w;     // [T][k]
+  const void* shared_out;  // [T][d] or nullptr
+  void* out;               // [T][d]
+  int32_t T, k, d;
+};
+hipError_t launch_combine(const CombineParams& p, bool bf16, hipStream_t s);
+
+// Number of compute units of the current device (cached per device).
+int device_cu_count();
+
+}  // namespace moe

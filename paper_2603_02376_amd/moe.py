@@ -1,0 +1,243 @@
+"""Python binding of libmoe.so: argument marshalling only.
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of the method: it checks tensor devices, dtypes and shapes, turns
+tensors into device pointers and torch streams into ``hipStream_t`` handles,
+and raises :class:`MoeError` on a non-zero status. PyTorch only provides
+device memory and streams. If the library is not built, loading fails loudly;
+there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmoe.so")
+
+MOE_F32, MOE_BF16 = 0, 1
+MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
+STATUS = {0: "MOE_OK", -1: "MOE_ERR_INVALID_ARG", -2: "MOE_ERR_UNSUPPORTED",
+          -3: "MOE_ERR_WORKSPACE", -4: "MOE_ERR_HIP"}
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class moe_config_t(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("E", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("n_groups", ctypes.c_int32), ("topk_groups", ctypes.c_int32), ("I", ctypes.c_int32),
+                ("n_shared", ctypes.c_int32), ("I_shared", ctypes.c_int32), ("score", ctypes.c_int32),
+                ("renorm", ctypes.c_int32), ("route_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class moe_layer_debug_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("logits", "topk_idx", "topk_w", "counts", "offsets",
+                                               "sorted_token", "sorted_assign", "inv_perm", "y_perm",
+                                               "shared_out")]
+
+
+_VP, _I32, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+_CFG = ctypes.POINTER(moe_config_t)
+_SIGS = {
+    "moe_workspace_size": (_SZ, [_CFG, _I32]),
+    "moe_route": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "moe_dispatch": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "moe_expert_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "moe_shared_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "moe_combine": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "moe_layer": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ,
+                                 _VP, _VP, ctypes.POINTER(moe_layer_debug_t)]),
+    "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "moe_last_error": (ctypes.c_char_p, []),
+    "moe_version": (ctypes.c_char_p, []),
+}
+EXPORTS = tuple(_SIGS)
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmoe.so (once). Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(there is no fallback implementation)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise MoeError(status, lib().moe_last_error().decode())
+
+
+# ---------------------------------------------------------------------------
+# configuration
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class MoeConfig:
+    d: int
+    E: int
+    k: int
+    I: int
+    n_groups: int = 1
+    topk_groups: int = 1
+    n_shared: int = 0
+    I_shared: int = 0
+    score: str = "softmax"     # "softmax" | "sigmoid"
+    renorm: bool = True
+    scale: float = 1.0
+    dtype: str = "bf16"        # "bf16" | "f32"
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    def c(self) -> moe_config_t:
+        return moe_config_t(self.d, self.E, self.k, self.n_groups, self.topk_groups, self.I, self.n_shared,
+                            self.I_shared, MOE_SCORE_SIGMOID if self.score == "sigmoid" else MOE_SCORE_SOFTMAX,
+                            int(bool(self.renorm)), float(self.scale),
+                            MOE_BF16 if self.dtype == "bf16" else MOE_F32)
+
+
+def workspace_size(cfg: MoeConfig, T: int) -> int:
+    c = cfg.c()
+    return int(lib().moe_workspace_size(ctypes.byref(c), T))
+
+
+def alloc_workspace(cfg: MoeConfig, T: int, device="cuda") -> torch.Tensor:
+    n = workspace_size(cfg, T)
+    if n == 0:
+        raise MoeError(-1, lib().moe_last_error().decode() or "invalid config")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _ptr(t, name, dtype=None, numel=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs {numel}")
+    return t.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, torch.cuda.Stream):
+        return s.cuda_stream
+    return int(s)
+
+
+# ---------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ---------------------------------------------------------------------------
+
+def moe_route(cfg: MoeConfig, T, x, w_router, bias, logits, topk_idx, topk_w, stream=None):
+    c = cfg.c()
+    dt = cfg.torch_dtype
+    _check(lib().moe_route(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
+                           _ptr(w_router, "w_router", dt, cfg.E * cfg.d) if x is not None else None,
+                           _ptr(bias, "bias", torch.float32, cfg.E),
+                           _ptr(logits, "logits", torch.float32, T * cfg.E),
+                           _ptr(topk_idx, "topk_idx", torch.int32, T * cfg.k),
+                           _ptr(topk_w, "topk_w", torch.float32, T * cfg.k), _stream(stream)))
+
+
+def moe_dispatch(cfg: MoeConfig, T, topk_idx, counts, offsets, sorted_token, sorted_assign, inv_perm, ws,
+                 stream=None):
+    c = cfg.c()
+    n = T * cfg.k
+    _check(lib().moe_dispatch(ctypes.byref(c), T, _ptr(topk_idx, "topk_idx", torch.int32, n),
+                              _ptr(counts, "counts", torch.int32, cfg.E),
+                              _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                              _ptr(sorted_token, "sorted_token", torch.int32, n),
+                              _ptr(sorted_assign, "sorted_assign", torch.int32, n),
+                              _ptr(inv_perm, "inv_perm", torch.int32, n),
+                              _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_expert_ffn(cfg: MoeConfig, T, x, sorted_token, offsets, w_gate, w_up, w_down, y_perm, ws, stream=None):
+    c = cfg.c()
+    dt = cfg.torch_dtype
+    n = T * cfg.k
+    wsz = cfg.E * cfg.I * cfg.d
+    _check(lib().moe_expert_ffn(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
+                                _ptr(sorted_token, "sorted_token", torch.int32, n),
+                                _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                                _ptr(w_gate, "w_gate", dt, wsz), _ptr(w_up, "w_up", dt, wsz),
+                                _ptr(w_down, "w_down", dt, wsz), _ptr(y_perm, "y_perm", dt, n * cfg.d),
+                                _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_shared_ffn(cfg: MoeConfig, T, x, ws_gate, ws_up, ws_down, out, ws, stream=None):
+    c = cfg.c()
+    dt = cfg.torch_dtype
+    wsz = cfg.I_shared * cfg.d
+    _check(lib().moe_shared_ffn(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
+                                _ptr(ws_gate, "ws_gate", dt, wsz), _ptr(ws_up, "ws_up", dt, wsz),
+                                _ptr(ws_down, "ws_down", dt, wsz), _ptr(out, "out", dt, T * cfg.d),
+                                _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_combine(cfg: MoeConfig, T, y_perm, inv_perm, topk_w, shared_out, out, stream=None):
+    c = cfg.c()
+    dt = cfg.torch_dtype
+    n = T * cfg.k
+    _check(lib().moe_combine(ctypes.byref(c), T, _ptr(y_perm, "y_perm", dt, n * cfg.d),
+                             _ptr(inv_perm, "inv_perm", torch.int32, n),
+                             _ptr(topk_w, "topk_w", torch.float32, n),
+                             _ptr(shared_out, "shared_out", dt, T * cfg.d),
+                             _ptr(out, "out", dt, T * cfg.d), _stream(stream)))
+
+
+def moe_layer(cfg: MoeConfig, T, x, w_router, bias, w_gate, w_up, w_down, ws_gate, ws_up, ws_down, out, ws,
+              s_main=None, s_aux=None, dbg: dict | None = None):
+    """The whole layer; ``dbg`` maps intermediate names to device tensors that
+    receive them (keys as in ``moe_layer_debug_t``)."""
+    c = cfg.c()
+    dt = cfg.torch_dtype
+    wsz = cfg.E * cfg.I * cfg.d
+    swsz = cfg.I_shared * cfg.d
+    dbg_s = None
+    if dbg:
+        unknown = set(dbg) - {f for f, _ in moe_layer_debug_t._fields_}
+        if unknown:
+            raise KeyError(f"unknown debug buffers {sorted(unknown)}")
+        dbg_s = moe_layer_debug_t(**{k: _ptr(v, k) for k, v in dbg.items()})
+    _check(lib().moe_layer(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
+                           _ptr(w_router, "w_router", dt, cfg.E * cfg.d), _ptr(bias, "bias", torch.float32, cfg.E),
+                           _ptr(w_gate, "w_gate", dt, wsz), _ptr(w_up, "w_up", dt, wsz),
+                           _ptr(w_down, "w_down", dt, wsz), _ptr(ws_gate, "ws_gate", dt, swsz),
+                           _ptr(ws_up, "ws_up", dt, swsz), _ptr(ws_down, "ws_down", dt, swsz),
+                           _ptr(out, "out", dt, T * cfg.d), _ptr(ws, "ws"), ws.numel() * ws.element_size(),
+                           _stream(s_main), _stream(s_aux) if s_aux is not None else None,
+                           ctypes.byref(dbg_s) if dbg_s is not None else None))
+
+
+def version() -> str:
+    return lib().moe_version().decode()

@@ -1,0 +1,224 @@
+"""Per-call GPU parity: every C-ABI entry point against the CPU oracle.
+
+Integer results (routing indices, counts, offsets, permutation) must match
+bit for bit; floating-point results must stay within the tolerance of their
+precision (bf16 2e-2, fp32 1e-5, as max |got - want| / max(|want|, rms(want))).
+Shapes span several tiles with ragged tails, and include empty experts, a hot
+expert, T = 1 and every GEMM tile configuration the library selects.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from oracle.checks import check_dispatch, max_rel_err
+from paper_2603_02376_amd import inputs, moe
+from tests.gpu_util import BF16_TOL, F32_TOL, LOGIT_TOL, WEIGHT_TOL, host, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t if dtype is None else t.to(dtype)
+
+
+# ---------------------------------------------------------------------------
+# moe_route
+# ---------------------------------------------------------------------------
+
+ROUTE_CASES = [
+    # T, E, k, G, TG, score, bias, renorm, scale
+    (1, 8, 2, 1, 1, "softmax", False, True, 1.0),
+    (17, 8, 2, 1, 1, "softmax", False, True, 1.0),
+    (300, 64, 6, 1, 1, "softmax", False, False, 1.0),
+    (257, 64, 4, 8, 3, "softmax", False, True, 1.0),
+    (1000, 256, 8, 8, 4, "sigmoid", True, True, 2.5),
+    (4096, 256, 8, 8, 4, "sigmoid", False, True, 2.5),
+    (129, 96, 5, 4, 2, "sigmoid", True, False, 1.5),
+    (64, 12, 4, 3, 2, "sigmoid", True, True, 1.0),
+    (33, 256, 16, 1, 1, "sigmoid", True, True, 2.5),
+    (50, 4, 4, 1, 1, "softmax", False, True, 1.0),       # k = E
+]
+
+
+@pytest.mark.parametrize("case", ROUTE_CASES, ids=lambda c: "T{}_E{}_k{}_G{}".format(*c[:4]))
+@pytest.mark.parametrize("ties", [False, True])
+def test_route_bit_exact(case, ties):
+    T, E, k, G, TG, score, use_bias, renorm, scale = case
+    log("route", case, "ties", ties)
+    rng = np.random.default_rng(T * 7 + E)
+    u = rng.normal(scale=1.7, size=(T, E)).astype(np.float32)
+    if ties:
+        u = (np.round(u * 2) / 2).astype(np.float32)   # many exact ties
+    bias = rng.normal(scale=0.1, size=E).astype(np.float32) if use_bias else None
+    if ties and bias is not None:
+        bias = (np.round(bias * 4) / 4).astype(np.float32)
+    cfg = moe.MoeConfig(d=64, E=E, k=k, I=64, n_groups=G, topk_groups=TG, score=score, renorm=renorm,
+                        scale=scale, dtype="f32")
+    logits = _dev(u)
+    idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    moe.moe_route(cfg, T, None, None, None if bias is None else _dev(bias), logits, idx, w)
+    torch.cuda.synchronize()
+    want_idx, want_w = O.route(u, k=k, score=score, bias=bias, n_groups=G, topk_groups=TG, renorm=renorm,
+                               scale=scale)
+    got_idx = host(idx)
+    bad = np.nonzero((got_idx != want_idx).any(axis=1))[0]
+    assert bad.size == 0, f"tokens {bad[:5]}: got {got_idx[bad[:2]]} want {want_idx[bad[:2]]}"
+    assert np.abs(host(w) - want_w).max() <= WEIGHT_TOL * max(1.0, scale)
+
+
+def test_route_all_equal_logits():
+    T, E, k = 10, 256, 8
+    cfg = moe.MoeConfig(d=64, E=E, k=k, I=64, n_groups=8, topk_groups=4, score="sigmoid", scale=2.5, dtype="f32")
+    logits = torch.full((T, E), 0.25, device="cuda")
+    idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    moe.moe_route(cfg, T, None, None, None, logits, idx, w)
+    torch.cuda.synchronize()
+    assert (host(idx) == np.arange(k)).all()
+    assert np.allclose(host(w), 2.5 / k, atol=1e-7)
+
+
+@pytest.mark.parametrize("T,d,E,dtype", [(1, 128, 8, "bf16"), (300, 4096, 8, "bf16"), (129, 7168, 256, "bf16"),
+                                         (64, 128, 8, "f32"), (77, 256, 40, "f32")])
+def test_gate_logits(T, d, E, dtype):
+    log("gate", T, d, E, dtype)
+    p = dict(T=T, d=d, E=E, bias="none")
+    x, wr, _ = inputs.host_activations(p, 3)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    xt, wt = _dev(x, tdt), _dev(wr, tdt)
+    cfg = moe.MoeConfig(d=d, E=E, k=2, I=64, dtype=dtype)
+    logits = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    idx = torch.empty((T, 2), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, 2), dtype=torch.float32, device="cuda")
+    moe.moe_route(cfg, T, xt, wt, None, logits, idx, w)
+    torch.cuda.synchronize()
+    want = O.gate_logits(inputs.oracle_view(xt), inputs.oracle_view(wt))
+    rms = np.sqrt(np.mean(want ** 2))
+    assert np.abs(host(logits) - want).max() / rms <= LOGIT_TOL
+    want_idx, _ = O.route(host(logits), k=2)
+    assert (host(idx) == want_idx).all()
+
+
+# ---------------------------------------------------------------------------
+# moe_dispatch
+# ---------------------------------------------------------------------------
+
+def _random_topk(T, E, k, rng, hot=None, pool=None):
+    """k distinct experts per token: from `pool` experts only (the others stay
+    empty), or `hot` first and k-1 others."""
+    n = E if pool is None else pool
+    idx = np.argsort(rng.random((T, n)), axis=1)[:, :k].astype(np.int32)
+    if hot is not None:
+        rest = np.argsort(rng.random((T, E - 1)), axis=1)[:, : k - 1]
+        rest = rest + (rest >= hot)
+        idx = np.concatenate([np.full((T, 1), hot), rest], axis=1).astype(np.int32)
+    return idx
+
+
+@pytest.mark.parametrize("T,E,k,hot", [(1, 8, 2, None), (3, 5, 2, None), (64, 8, 2, None), (65, 8, 8, None),
+                                       (1000, 64, 4, None), (4096, 256, 8, None), (4096, 256, 8, 17),
+                                       (777, 256, 1, None), (128, 256, 8, None), (5000, 16, 16, 3)])
+def test_dispatch_bit_exact(T, E, k, hot):
+    log("dispatch", T, E, k, hot)
+    rng = np.random.default_rng(T + E + k)
+    pool = E // 2 if (hot is None and E > 16) else None   # leave half the experts empty
+    idx = _random_topk(T, E, k, rng, hot, pool)
+    cfg = moe.MoeConfig(d=64, E=E, k=k, I=64, dtype="bf16")
+    ws = moe.alloc_workspace(cfg, T)
+    t_idx = _dev(idx)
+    outs = [torch.full((n,), -7, dtype=torch.int32, device="cuda") for n in (E, E + 1, T * k, T * k, T * k)]
+    moe.moe_dispatch(cfg, T, t_idx, *outs, ws)
+    torch.cuda.synchronize()
+    want = O.dispatch(idx, E)
+    for name, g, w in zip(("counts", "offsets", "sorted_token", "sorted_assign", "inv_perm"), outs, want):
+        assert np.array_equal(host(g), w), name
+    check_dispatch(idx, *(host(o) for o in (outs[0], outs[1], outs[2], outs[4], outs[3])))
+
+
+# ---------------------------------------------------------------------------
+# moe_expert_ffn / moe_shared_ffn
+# ---------------------------------------------------------------------------
+
+FFN_CASES = [
+    # T, d, E, k, I, dtype, hot  (avg rows/expert picks the tile configuration)
+    (1024, 256, 4, 2, 128, "bf16", None),     # avg 512 -> 256x256 tiles
+    (300, 320, 8, 2, 192, "bf16", None),      # avg 75  -> 128x256, ragged N tails
+    (100, 256, 16, 4, 128, "bf16", None),     # avg 25  -> 64x128
+    (50, 192, 64, 4, 320, "bf16", None),      # avg 3   -> 32x256, many empty experts
+    (1, 128, 8, 2, 64, "bf16", None),
+    (200, 128, 32, 4, 128, "bf16", 5),        # one hot expert (all 200 tokens)
+    (64, 128, 8, 2, 256, "f32", None),
+    (45, 192, 6, 3, 128, "f32", None),
+]
+
+
+def _ffn_inputs(T, d, E, k, I, dtype, hot, seed=0):
+    p = dict(T=T, d=d, E=E, k=k, I=I, dtype=dtype, n_shared=0, bias="none")
+    t = inputs.make_inputs(p, seed, "cuda")
+    rng = np.random.default_rng(seed + T)
+    idx = _random_topk(T, E, k, rng, hot)
+    return p, t, idx
+
+
+@pytest.mark.parametrize("case", FFN_CASES, ids=lambda c: "T{}_d{}_E{}_k{}_I{}_{}".format(*c[:6]))
+def test_expert_ffn(case):
+    T, d, E, k, I, dtype, hot = case
+    log("expert_ffn", case)
+    p, t, idx = _ffn_inputs(*case)
+    counts, offsets, st, sa, inv = O.dispatch(idx, E)
+    cfg = moe.MoeConfig(d=d, E=E, k=k, I=I, dtype=dtype)
+    ws = moe.alloc_workspace(cfg, T)
+    y = torch.full((T * k, d), float("nan"), dtype=t["x"].dtype, device="cuda")
+    moe.moe_expert_ffn(cfg, T, t["x"], _dev(st), _dev(offsets), t["w_gate"], t["w_up"], t["w_down"], y, ws)
+    torch.cuda.synchronize()
+    want = O.expert_ffn(inputs.oracle_view(t["x"]), st, offsets, inputs.ExpertView(t["w_gate"]),
+                        inputs.ExpertView(t["w_up"]), inputs.ExpertView(t["w_down"]))
+    got = host(y.float())
+    assert np.isfinite(got).all(), "rows left unwritten"
+    err = max_rel_err(got, want)
+    log("  max_rel_err", err)
+    assert err <= (BF16_TOL if dtype == "bf16" else F32_TOL)
+
+
+@pytest.mark.parametrize("T,d,Is,dtype", [(1, 128, 64, "bf16"), (300, 320, 192, "bf16"), (1000, 512, 256, "bf16"),
+                                          (33, 128, 128, "f32")])
+def test_shared_ffn(T, d, Is, dtype):
+    log("shared_ffn", T, d, Is, dtype)
+    p = dict(T=T, d=d, E=1, k=1, I=64, dtype=dtype, n_shared=1, I_shared=Is, bias="none")
+    t = inputs.make_inputs(p, 1, "cuda")
+    cfg = moe.MoeConfig(d=d, E=1, k=1, I=64, n_shared=1, I_shared=Is, dtype=dtype)
+    ws = moe.alloc_workspace(cfg, T)
+    out = torch.empty((T, d), dtype=t["x"].dtype, device="cuda")
+    moe.moe_shared_ffn(cfg, T, t["x"], t["ws_gate"], t["ws_up"], t["ws_down"], out, ws)
+    torch.cuda.synchronize()
+    want = O.swiglu_ffn(inputs.oracle_view(t["x"]), inputs.oracle_view(t["ws_gate"]),
+                        inputs.oracle_view(t["ws_up"]), inputs.oracle_view(t["ws_down"]))
+    assert max_rel_err(host(out.float()), want) <= (BF16_TOL if dtype == "bf16" else F32_TOL)
+
+
+# ---------------------------------------------------------------------------
+# moe_combine
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,d,k,dtype,shared", [(1, 64, 1, "bf16", False), (100, 7168, 8, "bf16", True),
+                                                (257, 4096, 2, "bf16", False), (64, 128, 2, "f32", False),
+                                                (31, 192, 16, "f32", True)])
+def test_combine(T, d, k, dtype, shared):
+    log("combine", T, d, k, dtype, shared)
+    rng = np.random.default_rng(T * d + k)
+    n = T * k
+    perm = rng.permutation(n).astype(np.int32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    y = _dev(rng.normal(size=(n, d)).astype(np.float32), tdt)
+    w = rng.random((T, k)).astype(np.float32)
+    sh = _dev(rng.normal(size=(T, d)).astype(np.float32), tdt) if shared else None
+    cfg = moe.MoeConfig(d=d, E=max(k, 2), k=k, I=64, dtype=dtype)
+    out = torch.empty((T, d), dtype=tdt, device="cuda")
+    moe.moe_combine(cfg, T, y, _dev(perm), _dev(w), sh, out)
+    torch.cuda.synchronize()
+    want = O.combine(inputs.oracle_view(y), perm, w, inputs.oracle_view(sh))
+    tol = 8e-3 if dtype == "bf16" else F32_TOL   # one bf16 rounding of the output
+    assert max_rel_err(host(out.float()), want) <= tol
