@@ -65,7 +65,8 @@ def measured_traffic(workload: str):
     return rec.get("bytes_per_call")
 
 
-def run_workload(name: str, steps: int, warmup: int, want_cpu: bool):
+def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens: int = 64,
+                 ffn_only: bool = False):
     import numpy as np
     import torch
 
@@ -99,19 +100,21 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool):
     counts = dbg["counts"].cpu().numpy()
     alg = algorithmic(p, counts)
 
-    for _ in range(warmup):
-        layer()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    log(f"[bench] {name}: timing {steps} layer steps")
-    wall0 = time.perf_counter()
-    e0.record(s_main)
-    for _ in range(steps):
-        layer()
-    e1.record(s_main)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms = e0.elapsed_time(e1) / steps
+    ms = wall = float("nan")
+    if not ffn_only:
+        for _ in range(warmup):
+            layer()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        log(f"[bench] {name}: timing {steps} layer steps")
+        wall0 = time.perf_counter()
+        e0.record(s_main)
+        for _ in range(steps):
+            layer()
+        e1.record(s_main)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        ms = e0.elapsed_time(e1) / steps
 
     # dominant kernel pair: the grouped expert FFN, timed alone on its stream
     y = torch.empty((T * p["k"], p["d"]), dtype=cfg.torch_dtype, device="cuda")
@@ -120,6 +123,7 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool):
         moe.moe_expert_ffn(cfg, T, t["x"], dbg["sorted_token"], dbg["offsets"], t["w_gate"], t["w_up"],
                            t["w_down"], y, ws, stream=s_main)
 
+    log(f"[bench] {name}: timing {steps} expert-FFN calls")
     for _ in range(max(2, warmup)):
         ffn()
     torch.cuda.synchronize()
@@ -140,7 +144,8 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool):
         ffn_tflops=alg["ffn_flops"] / (ffn_ms / 1e3) / 1e12,
     )
     if want_cpu:
-        res["cpu"] = cpu_baseline(p, t)
+        log(f"[bench] {name}: CPU oracle baseline on {cpu_tokens} tokens")
+        res["cpu"] = cpu_baseline(p, t, cpu_tokens)
     del t, ws, out, y
     torch.cuda.empty_cache()
     return res
@@ -194,6 +199,11 @@ def main():
     ap.add_argument("--workload", default="dsv3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the mixtral and decode side measurements")
+    ap.add_argument("--cpu-tokens", type=int, default=64, help="tokens in the CPU-oracle baseline sample")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="first run 3 plain device copies of this many MiB (reference for HBM byte counters)")
+    ap.add_argument("--ffn-only", action="store_true",
+                    help="profiling aid: run only the timed expert-FFN loop of the workload and print its timing")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the layer is one GPU's share of the "
@@ -206,7 +216,24 @@ def main():
 
     moe.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
-    main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(3):
+            dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: 3 x {n} B, {2 * 3 * n / (c0.elapsed_time(c1) / 1e3) / 1e9:.1f} GB/s")
+        del src, dst
+    main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_tokens,
+                            args.ffn_only)
+    if args.ffn_only:
+        print(json.dumps(dict(workload=args.workload, expert_ffn_ms=main_res["ffn_ms"],
+                              expert_ffn_gbs=main_res["ffn_gbs"], expert_ffn_tflops=main_res["ffn_tflops"])))
+        return
     extra = {}
     if not args.no_extra:
         for name in ("dsv3_decode", "mixtral"):

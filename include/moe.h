@@ -111,7 +111,7 @@ size_t moe_workspace_size(const moe_config_t* cfg, int32_t T);
  * experts before the dispatch; selection rule as in the header comment).
  *  x, w_router : if x != NULL, logits = x · w_routerᵀ is computed (fp32
  *                accumulation) and written to `logits`; if x == NULL,
- *                `logits` is an input and w_router is ignored.
+ *                `logits` is an input and w_router and ws are ignored.
  *  bias        : [E] fp32 added to the sigmoid scores for selection only;
  *                may be NULL (no bias); must be NULL for softmax routing.
  *  logits      : [T][E] fp32, required.
@@ -120,12 +120,15 @@ size_t moe_workspace_size(const moe_config_t* cfg, int32_t T);
  *  topk_w      : [T][k] fp32 out: selected scores (softmax probabilities or
  *                unbiased sigmoid), divided by their sum if cfg->renorm, times
  *                cfg->route_scale.
+ *  ws          : workspace (required when x != NULL: the router GEMM may split
+ *                its reduction into fp32 partial sums, which the routing
+ *                kernel adds in a fixed order).
  * Keys, group scores and weights are evaluated in fp64 from the fp32 logits,
  * so the selection is a deterministic function of the logits' bits.
  */
 int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_router,
-              const float* bias, float* logits, int32_t* topk_idx, float* topk_w,
-              hipStream_t stream);
+              const float* bias, float* logits, int32_t* topk_idx, float* topk_w, void* ws,
+              size_t ws_bytes, hipStream_t stream);
 
 /*
  * moe_dispatch — the single-GPU form of the dispatch all-to-all (App. F,

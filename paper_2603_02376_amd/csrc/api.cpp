@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <mutex>
@@ -31,9 +32,21 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 size_t esize(const moe_config_t& c) { return c.dtype == MOE_BF16 ? 2 : 4; }
 
+// K-split of the router GEMM (bf16 only): enough 32-row tiles x splits to
+// occupy ~512 workgroups, at least 4 k-steps of 64 per split. A function of
+// (T, d) only, so the workspace size does not depend on the device.
+int gate_splits(const moe_config_t& c, int32_t T) {
+  if (c.dtype != MOE_BF16 || T <= 0) return 1;
+  const int mtiles = (T + 31) / 32;
+  const int nkt = c.d / 64;
+  int s = std::max(1, std::min(nkt / 4, (512 + mtiles - 1) / mtiles));
+  const int q = (nkt + s - 1) / s;
+  return (nkt + q - 1) / q;  // no empty split
+}
+
 // Byte offsets of every scratch region inside the caller's workspace.
 struct Layout {
-  size_t logits, topk_idx, topk_w, masks, bases, counts, offsets, sorted_token, sorted_assign,
+  size_t gate_partials, logits, topk_idx, topk_w, masks, bases, counts, offsets, sorted_token, sorted_assign,
       inv_perm, h, y_perm, shared_h, shared_out, total;
 };
 
@@ -47,6 +60,8 @@ Layout make_layout(const moe_config_t& c, int32_t T) {
   };
   const size_t t = (size_t)T, tk = (size_t)T * c.k, es = esize(c);
   const size_t nch = (t + moe::kDispatchChunk - 1) / moe::kDispatchChunk;
+  const int gs = gate_splits(c, T);
+  L.gate_partials = take(gs > 1 ? (size_t)gs * t * c.E * 4 : 0);
   L.logits = take(t * c.E * 4);
   L.topk_idx = take(tk * 4);
   L.topk_w = take(tk * 4);
@@ -124,25 +139,36 @@ hipError_t run_gemm(const moe_config_t& c, const moe::GemmProblem& p, int epi, b
   return moe::launch_gemm_f32(p, epi, s);
 }
 
-hipError_t run_gate(const moe_config_t& c, int32_t T, const void* x, const void* w_router, float* logits,
-                    hipStream_t s) {
-  moe::GemmProblem g{};
-  g.A = x;
-  g.a_rows = T;
-  g.groups = 1;
-  g.M = T;
-  g.B0 = w_router;
-  g.N = c.E;
-  g.K = c.d;
-  g.C = logits;
-  g.ldc = c.E;
-  return run_gemm(c, g, moe::EPI_STORE, true, s);
-}
-
-hipError_t run_route(const moe_config_t& c, int32_t T, const float* bias, const float* logits, int32_t* idx,
-                     float* w, hipStream_t s) {
+// Router GEMM then routing. With a K split the GEMM writes fp32 partial
+// logits to `partials` and the route kernel sums them (in a fixed order) into
+// `logits`; without one the GEMM writes `logits` directly. x == nullptr: the
+// logits are an input.
+hipError_t run_gate_route(const moe_config_t& c, int32_t T, const void* x, const void* w_router,
+                          const float* bias, float* logits, float* partials, int32_t* idx, float* w,
+                          hipStream_t s) {
+  const int splits = x ? gate_splits(c, T) : 1;
+  if (x) {
+    moe::GemmProblem g{};
+    g.A = x;
+    g.a_rows = T;
+    g.groups = 1;
+    g.M = T;
+    g.B0 = w_router;
+    g.N = c.E;
+    g.K = c.d;
+    g.C = splits > 1 ? partials : logits;
+    g.ldc = c.E;
+    g.ksplit = splits;
+    g.c_split_stride = (int64_t)T * c.E;
+    g.tile = moe::GEMM_TILE_SKINNY;
+    const hipError_t e = run_gemm(c, g, moe::EPI_STORE, true, s);
+    if (e != hipSuccess) return e;
+  }
   moe::RouteParams r{};
-  r.logits = logits;
+  r.logits_in = splits > 1 ? partials : logits;
+  r.nsplit = splits;
+  r.split_stride = (int64_t)T * c.E;
+  r.logits_out = splits > 1 ? logits : nullptr;
   r.bias = (c.score == MOE_SCORE_SIGMOID) ? bias : nullptr;
   r.T = T;
   r.E = c.E;
@@ -274,7 +300,7 @@ size_t moe_workspace_size(const moe_config_t* cfg, int32_t T) {
 }
 
 int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_router, const float* bias,
-              float* logits, int32_t* topk_idx, float* topk_w, hipStream_t stream) {
+              float* logits, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream) {
   MOE_CHECK(validate(cfg, T));
   if (cfg->score == MOE_SCORE_SOFTMAX && bias) return fail(MOE_ERR_INVALID_ARG, "bias given for softmax routing");
   MOE_CHECK(need(logits, "logits"));
@@ -283,12 +309,12 @@ int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   if (x) {
     MOE_CHECK(need(x, "x"));
     MOE_CHECK(need(w_router, "w_router"));
+    MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   }
   if (T == 0) return MOE_OK;
-  hipError_t e;
-  if (x && (e = run_gate(*cfg, T, x, w_router, logits, stream)) != hipSuccess) return hip_fail(e, "gate GEMM");
-  if ((e = run_route(*cfg, T, bias, logits, topk_idx, topk_w, stream)) != hipSuccess) return hip_fail(e, "route");
-  return MOE_OK;
+  float* partials = x ? reinterpret_cast<float*>(static_cast<char*>(ws) + make_layout(*cfg, T).gate_partials) : nullptr;
+  const hipError_t e = run_gate_route(*cfg, T, x, w_router, bias, logits, partials, topk_idx, topk_w, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "route");
 }
 
 int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, int32_t* counts, int32_t* offsets,
@@ -411,8 +437,9 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
       return hip_fail(e, "shared FFN");
     if ((e = hipEventRecord(ev->join, s_aux)) != hipSuccess) return hip_fail(e, "event record");
   }
-  if ((e = run_gate(c, T, x, w_router, logits, s_main)) != hipSuccess) return hip_fail(e, "gate GEMM");
-  if ((e = run_route(c, T, bias, logits, idx, tw, s_main)) != hipSuccess) return hip_fail(e, "route");
+  if ((e = run_gate_route(c, T, x, w_router, bias, logits, reinterpret_cast<float*>(w + L.gate_partials), idx, tw,
+                          s_main)) != hipSuccess)
+    return hip_fail(e, "route");
   if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main)) != hipSuccess)
     return hip_fail(e, "dispatch");
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main)) != hipSuccess)

@@ -12,6 +12,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
+// Tile shape of the bf16 grouped GEMM: chosen from the rows per group, or
+// the skinny 32x256 shape (used by the router GEMM, whose N is the expert
+// count).
+enum GemmTile : int { GEMM_TILE_AUTO = 0, GEMM_TILE_SKINNY = 1 };
+
 // Epilogue of the grouped GEMM.
 enum GemmEpilogue : int {
   EPI_STORE = 0,   // C = A·Bᵀ
@@ -40,6 +45,11 @@ struct GemmProblem {
   int32_t K;
   void* C;
   int32_t ldc;
+  // K split (bf16 EPI_STORE with fp32 output only): split s sums the k-steps
+  // [s*q, (s+1)*q), q = ceil(K/64 / ksplit), into C + s*c_split_stride.
+  int32_t ksplit;
+  int64_t c_split_stride;
+  int32_t tile;  // GemmTile
 };
 
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
@@ -49,7 +59,12 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, int epilogue, bool out_f32, hi
 hipError_t launch_gemm_f32(const GemmProblem& p, int epilogue, hipStream_t s);
 
 struct RouteParams {
-  const float* logits;  // [T][E]
+  // logits = sum over s < nsplit of logits_in[s*split_stride + t*E + e],
+  // summed in ascending s; written to logits_out when that is not null.
+  const float* logits_in;
+  int32_t nsplit;
+  int64_t split_stride;
+  float* logits_out;
   const float* bias;    // [E] or nullptr
   int32_t T, E, k, n_groups, topk_groups, score, renorm;
   float scale;

@@ -7,7 +7,9 @@
 // (softmax, top-k, renormalised).
 //
 // Lane l holds experts [l*EPL, l*EPL + EPL) (EPL = ceil(E/64) <= 4), so the
-// logits of a token are read with one coalesced load per lane. Keys, group
+// logits of a token are read with one coalesced load per lane. When the
+// router GEMM was split along K, the kernel first sums the partial logits in
+// a fixed order (and stores the sums), so the logits stay deterministic. Keys, group
 // scores and weights are evaluated in fp64: the selection is then a
 // deterministic function of the fp32 logits' bits and a near-tie in fp32
 // cannot flip it. Group scores (sum of a group's two largest keys) come from
@@ -71,7 +73,14 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
   for (int i = 0; i < EPL; ++i) {
     const int e = lane * EPL + i;
     const bool ok = active && e < E;
-    u[i] = ok ? p.logits[(size_t)t * E + e] : 0.f;
+    float v = 0.f;
+    if (ok) {
+      const float* src = p.logits_in + (size_t)t * E + e;
+      v = src[0];
+      for (int sp = 1; sp < p.nsplit; ++sp) v += src[(size_t)sp * p.split_stride];
+      if (p.logits_out) p.logits_out[(size_t)t * E + e] = v;
+    }
+    u[i] = v;
     if (!ok) {
       key[i] = NEG;
       score[i] = 0.0;

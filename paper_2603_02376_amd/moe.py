@@ -47,7 +47,7 @@ _VP, _I32, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
 _CFG = ctypes.POINTER(moe_config_t)
 _SIGS = {
     "moe_workspace_size": (_SZ, [_CFG, _I32]),
-    "moe_route": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "moe_route": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_dispatch": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_expert_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_shared_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
@@ -157,7 +157,9 @@ def _stream(s):
 # entry points (same names as the C ABI)
 # ---------------------------------------------------------------------------
 
-def moe_route(cfg: MoeConfig, T, x, w_router, bias, logits, topk_idx, topk_w, stream=None):
+def moe_route(cfg: MoeConfig, T, x, w_router, bias, logits, topk_idx, topk_w, ws=None, stream=None):
+    """x = None routes from the given logits; otherwise the router GEMM runs
+    first and ``ws`` (see :func:`alloc_workspace`) is required."""
     c = cfg.c()
     dt = cfg.torch_dtype
     _check(lib().moe_route(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
@@ -165,7 +167,8 @@ def moe_route(cfg: MoeConfig, T, x, w_router, bias, logits, topk_idx, topk_w, st
                            _ptr(bias, "bias", torch.float32, cfg.E),
                            _ptr(logits, "logits", torch.float32, T * cfg.E),
                            _ptr(topk_idx, "topk_idx", torch.int32, T * cfg.k),
-                           _ptr(topk_w, "topk_w", torch.float32, T * cfg.k), _stream(stream)))
+                           _ptr(topk_w, "topk_w", torch.float32, T * cfg.k), _ptr(ws, "ws"),
+                           0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def moe_dispatch(cfg: MoeConfig, T, topk_idx, counts, offsets, sorted_token, sorted_assign, inv_perm, ws,

@@ -75,7 +75,7 @@ def test_invalid_configs_rejected(kw, status):
     cfg = _cfg(**kw)
     assert moe.workspace_size(cfg, 16) == 0
     c = cfg.c()
-    r = moe.lib().moe_route(ctypes.byref(c), 16, None, None, None, FAKE, FAKE, FAKE, None)
+    r = moe.lib().moe_route(ctypes.byref(c), 16, None, None, None, FAKE, FAKE, FAKE, None, 0, None)
     assert r == status
     assert moe.lib().moe_last_error().decode()
 
@@ -83,15 +83,18 @@ def test_invalid_configs_rejected(kw, status):
 def test_null_and_negative_arguments():
     c = _cfg().c()
     L = moe.lib()
-    assert L.moe_route(None, 4, None, None, None, FAKE, FAKE, FAKE, None) == -1
-    assert L.moe_route(ctypes.byref(c), -1, None, None, None, FAKE, FAKE, FAKE, None) == -1
-    assert L.moe_route(ctypes.byref(c), 4, None, None, None, None, FAKE, FAKE, None) == -1
+    assert L.moe_route(None, 4, None, None, None, FAKE, FAKE, FAKE, None, 0, None) == -1
+    assert L.moe_route(ctypes.byref(c), -1, None, None, None, FAKE, FAKE, FAKE, None, 0, None) == -1
+    assert L.moe_route(ctypes.byref(c), 4, None, None, None, None, FAKE, FAKE, None, 0, None) == -1
     assert b"logits" in L.moe_last_error()
     # misaligned pointer
-    assert L.moe_route(ctypes.byref(c), 4, None, None, None, FAKE + 4, FAKE, FAKE, None) == -1
+    assert L.moe_route(ctypes.byref(c), 4, None, None, None, FAKE + 4, FAKE, FAKE, None, 0, None) == -1
     assert b"aligned" in L.moe_last_error()
     # bias with softmax routing
-    assert L.moe_route(ctypes.byref(c), 4, None, None, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert L.moe_route(ctypes.byref(c), 4, None, None, FAKE, FAKE, FAKE, FAKE, None, 0, None) == -1
+    # router GEMM without a workspace
+    assert L.moe_route(ctypes.byref(c), 4, FAKE, FAKE, None, FAKE, FAKE, FAKE, None, 0, None) == -1
+    assert L.moe_route(ctypes.byref(c), 4, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, 16, None) == -3
     # combine / expert_ffn NULLs
     assert L.moe_combine(ctypes.byref(c), 4, None, FAKE, FAKE, None, FAKE, None) == -1
     assert L.moe_expert_ffn(ctypes.byref(c), 4, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None) == -1
@@ -116,7 +119,7 @@ def test_zero_tokens_is_a_noop():
     c = cfg.c()
     L = moe.lib()
     need = moe.workspace_size(cfg, 0)
-    assert L.moe_route(ctypes.byref(c), 0, None, None, None, FAKE, FAKE, FAKE, None) == 0
+    assert L.moe_route(ctypes.byref(c), 0, None, None, None, FAKE, FAKE, FAKE, None, 0, None) == 0
     assert L.moe_dispatch(ctypes.byref(c), 0, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, need, None) == 0
     assert L.moe_combine(ctypes.byref(c), 0, FAKE, FAKE, FAKE, None, FAKE, None) == 0
     assert L.moe_layer(ctypes.byref(c), 0, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,

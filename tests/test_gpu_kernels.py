@@ -93,7 +93,7 @@ def test_gate_logits(T, d, E, dtype):
     logits = torch.empty((T, E), dtype=torch.float32, device="cuda")
     idx = torch.empty((T, 2), dtype=torch.int32, device="cuda")
     w = torch.empty((T, 2), dtype=torch.float32, device="cuda")
-    moe.moe_route(cfg, T, xt, wt, None, logits, idx, w)
+    moe.moe_route(cfg, T, xt, wt, None, logits, idx, w, ws=moe.alloc_workspace(cfg, T))
     torch.cuda.synchronize()
     want = O.gate_logits(inputs.oracle_view(xt), inputs.oracle_view(wt))
     rms = np.sqrt(np.mean(want ** 2))
