@@ -40,6 +40,8 @@
  *    to nearest even). dtype MOE_F32: fp32 throughout.
  *  - Supported: 1 <= E <= 256, 1 <= k <= min(E, 16), d and I multiples of 64,
  *    n_shared in {0, 1}; larger or other shapes return MOE_ERR_UNSUPPORTED.
+ *    The routed-expert weights are row-major unless cfg->weight_layout is
+ *    MOE_LAYOUT_PACKED (see moe_pack_weights).
  *    Inputs must be finite.
  *  - Results are deterministic: two calls on the same inputs give the same
  *    bits, whatever the stream arrangement (no atomics decide any order).
@@ -71,6 +73,14 @@ typedef enum {
   MOE_SCORE_SIGMOID = 1  /* DeepSeek-V3: sigmoid scores, selection on s + bias  */
 } moe_score_t;
 
+/* Layout of the routed-expert weights passed to moe_expert_ffn / moe_layer. */
+typedef enum {
+  MOE_LAYOUT_ROWMAJOR = 0, /* w_gate, w_up [E][I][d]; w_down [E][d][I]                       */
+  MOE_LAYOUT_PACKED = 1    /* from moe_pack_weights: w_gate = packed gate+up, w_up = NULL,
+                              w_down = packed down; bf16 only, I % 128 == 0, d % 256 == 0,
+                              T*d and T*k*I below 2^31 elements                               */
+} moe_layout_t;
+
 typedef struct {
   int32_t d;           /* hidden size                                         */
   int32_t E;           /* routed experts                                      */
@@ -84,6 +94,7 @@ typedef struct {
   int32_t renorm;      /* 1: divide the selected scores by their sum          */
   float route_scale;   /* multiplies every weight (1.0 Mixtral, 2.5 DSV3)     */
   int32_t dtype;       /* moe_dtype_t                                         */
+  int32_t weight_layout; /* moe_layout_t of the routed-expert weights          */
 } moe_config_t;
 
 /* Optional device buffers moe_layer writes its intermediates into (each may be
@@ -197,6 +208,27 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
               const float* bias, const void* w_gate, const void* w_up, const void* w_down,
               const void* ws_gate, const void* ws_up, const void* ws_down, void* out, void* ws,
               size_t ws_bytes, hipStream_t s_main, hipStream_t s_aux, moe_layer_debug_t* dbg);
+
+/*
+ * moe_pack_weights — one-time conversion of the routed-expert weights into
+ * the packed layout read by the weight-streaming expert GEMMs (a layout
+ * choice of this library, not of the paper: it makes each K step of a
+ * workgroup's weights one contiguous block already in matrix-core operand
+ * order, so the memory-bound expert FFN streams the weights linearly).
+ *  w_gate, w_up : [E][I][d] row-major bf16; gate_up_packed: 2*E*I*d bf16 out
+ *                 (NULL: skipped).
+ *  w_down       : [E][d][I] row-major bf16; down_packed: E*d*I bf16 out
+ *                 (NULL: skipped).
+ * cfg->weight_layout is ignored; requires bf16, I % 128 == 0, d % 256 == 0.
+ * Packed layout per expert (8 bf16 per 16-byte chunk, k = s*64 + kk*16 +
+ * 8*(lane >= 32) + 0..7):
+ *  gate_up: [I/128][d/64 s][4 w][4 kk][2 j][64 lane][8], column
+ *           t*128 + w*32 + lane%32 of w_gate (j = 0) or w_up (j = 1);
+ *  down:    [d/256][I/64 s][4 w][4 kk][2 j][64 lane][8], output column
+ *           t*256 + w*64 + j*32 + lane%32.
+ */
+int moe_pack_weights(const moe_config_t* cfg, const void* w_gate, const void* w_up, const void* w_down,
+                     void* gate_up_packed, void* down_packed, hipStream_t stream);
 
 /* Static text for a moe_status_t. */
 const char* moe_status_string(int status);

@@ -105,6 +105,15 @@ int validate(const moe_config_t* c, int32_t T) {
   if (c->d % 64 != 0 || c->I % 64 != 0 || (c->n_shared && c->I_shared % 64 != 0))
     return fail(MOE_ERR_UNSUPPORTED, "d, I and I_shared must be multiples of 64");
   if ((int64_t)T * c->k >= (int64_t)1 << 31) return fail(MOE_ERR_UNSUPPORTED, "T*k >= 2^31");
+  if (c->weight_layout != MOE_LAYOUT_ROWMAJOR && c->weight_layout != MOE_LAYOUT_PACKED)
+    return fail(MOE_ERR_INVALID_ARG, "unknown weight layout");
+  if (c->weight_layout == MOE_LAYOUT_PACKED && (c->dtype != MOE_BF16 || c->I % 128 != 0 || c->d % 256 != 0))
+    return fail(MOE_ERR_UNSUPPORTED, "packed weights need bf16, I % 128 == 0 and d % 256 == 0");
+  // The weight-streaming GEMMs address their row operand (x, then the
+  // intermediate h) with 32-bit byte offsets.
+  if (c->weight_layout == MOE_LAYOUT_PACKED &&
+      ((int64_t)T * c->d * 2 > (int64_t)UINT32_MAX || (int64_t)T * c->k * c->I * 2 > (int64_t)UINT32_MAX))
+    return fail(MOE_ERR_UNSUPPORTED, "packed weights need T*d and T*k*I below 2^31 elements");
   return MOE_OK;
 }
 
@@ -204,7 +213,7 @@ hipError_t run_dispatch(const moe_config_t& c, int32_t T, const int32_t* idx, ch
 // y = h Wdᵀ into `y`.
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
-                   void* h, void* y, hipStream_t s) {
+                   void* h, void* y, hipStream_t s, bool packed = false) {
   moe::GemmProblem up{};
   up.A = x;
   up.a_rows = a_rows;
@@ -218,7 +227,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   up.K = c.d;
   up.C = h;
   up.ldc = inter;
-  hipError_t e = run_gemm(c, up, moe::EPI_SWIGLU, false, s);
+  hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
   if (e != hipSuccess) return e;
   moe::GemmProblem down{};
   down.A = h;
@@ -231,7 +240,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   down.K = inter;
   down.C = y;
   down.ldc = c.d;
-  return run_gemm(c, down, moe::EPI_STORE, false, s);
+  return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
 hipError_t run_combine(const moe_config_t& c, int32_t T, const void* y, const int32_t* inv, const float* w,
@@ -342,15 +351,16 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   MOE_CHECK(need(x, "x"));
   MOE_CHECK(need(sorted_token, "sorted_token"));
   MOE_CHECK(need(offsets, "offsets"));
+  const bool packed = cfg->weight_layout == MOE_LAYOUT_PACKED;
   MOE_CHECK(need(w_gate, "w_gate"));
-  MOE_CHECK(need(w_up, "w_up"));
+  if (!packed) MOE_CHECK(need(w_up, "w_up"));
   MOE_CHECK(need(w_down, "w_down"));
   MOE_CHECK(need(y_perm, "y_perm"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (T == 0) return MOE_OK;
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
-                               static_cast<char*>(ws) + L.h, y_perm, stream);
+                               static_cast<char*>(ws) + L.h, y_perm, stream, packed);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
 }
 
@@ -391,10 +401,11 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   MOE_CHECK(validate(cfg, T));
   const moe_config_t& c = *cfg;
   if (c.score == MOE_SCORE_SOFTMAX && bias) return fail(MOE_ERR_INVALID_ARG, "bias given for softmax routing");
+  const bool packed = c.weight_layout == MOE_LAYOUT_PACKED;
   MOE_CHECK(need(x, "x"));
   MOE_CHECK(need(w_router, "w_router"));
   MOE_CHECK(need(w_gate, "w_gate"));
-  MOE_CHECK(need(w_up, "w_up"));
+  if (!packed) MOE_CHECK(need(w_up, "w_up"));
   MOE_CHECK(need(w_down, "w_down"));
   MOE_CHECK(need(out, "out"));
   if (c.n_shared) {
@@ -442,7 +453,8 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     return hip_fail(e, "route");
   if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main)) != hipSuccess)
     return hip_fail(e, "dispatch");
-  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main)) != hipSuccess)
+  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main, packed)) !=
+      hipSuccess)
     return hip_fail(e, "expert FFN");
   if (c.n_shared) {
     if (two) {
@@ -453,6 +465,29 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     }
   }
   if ((e = run_combine(c, T, y, inv, tw, shared, out, s_main)) != hipSuccess) return hip_fail(e, "combine");
+  return MOE_OK;
+}
+
+int moe_pack_weights(const moe_config_t* cfg, const void* w_gate, const void* w_up, const void* w_down,
+                     void* gate_up_packed, void* down_packed, hipStream_t stream) {
+  if (!cfg) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
+  moe_config_t c = *cfg;
+  c.weight_layout = MOE_LAYOUT_PACKED;
+  MOE_CHECK(validate(&c, 0));
+  if (gate_up_packed) {
+    MOE_CHECK(need(w_gate, "w_gate"));
+    MOE_CHECK(need(w_up, "w_up"));
+    MOE_CHECK(need(gate_up_packed, "gate_up_packed"));
+  }
+  if (down_packed) {
+    MOE_CHECK(need(w_down, "w_down"));
+    MOE_CHECK(need(down_packed, "down_packed"));
+  }
+  hipError_t e;
+  if (gate_up_packed && (e = moe::launch_pack(w_gate, w_up, gate_up_packed, c.E, c.I, c.d, true, stream)) != hipSuccess)
+    return hip_fail(e, "pack gate/up");
+  if (down_packed && (e = moe::launch_pack(w_down, nullptr, down_packed, c.E, c.d, c.I, false, stream)) != hipSuccess)
+    return hip_fail(e, "pack down");
   return MOE_OK;
 }
 

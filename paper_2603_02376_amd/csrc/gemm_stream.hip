@@ -1,0 +1,403 @@
+// Weight-streaming grouped bf16 GEMM over packed expert weights (gfx950).
+//
+// The expert FFN of the MoE layer (App. M step 3; App. F GEMM1 + SwiGLU +
+// GEMM2) at DeepSeek-V3 shape is bound by reading every expert's weights
+// once: ~128 tokens per expert give ~128 FLOP per weight byte, below the
+// MI355X ridge. This kernel is organised around that stream:
+//
+//   * The weights are pre-packed (moe_pack_weights, once per model) so that a
+//     workgroup's weights for one 64-wide K step are one contiguous 32 KB
+//     block, already in the lane order of the MFMA B operand: each of the 4
+//     waves reads its 8 KB as eight fully coalesced 1 KB loads straight into
+//     registers. No LDS and no cross-wave sharing for B: waves own disjoint
+//     output columns.
+//   * Weights for kDepth-1 steps ahead stay in flight per wave (a ring of
+//     register sets, the K loop unrolled so every set is statically indexed).
+//   * The token rows (A, gathered through sorted_token) are shared by the 4
+//     waves through a two-slot LDS ring: each wave loads its share of the
+//     next step's rows into registers and writes them to the free slot at
+//     the end of the step; one barrier per step publishes them. Only
+//     register loads are in flight, so the compiler's load-count waits are
+//     exact. (Direct-to-LDS loads mixed with register loads under partial
+//     vmcnt waits were observed to read stale LDS data: their completions
+//     are not ordered with respect to each other.)
+//   * Within a step the instruction order is fixed: MFMAs interleaved with
+//     the LDS reads of the next 16-wide K slice and an even share of the
+//     step's loads, so a load waiting for queue space never idles the matrix
+//     core for long.
+//   * A pass covers up to 192 rows of one expert (the accumulators of 6 row
+//     fragments x 2 column fragments live in AGPRs, one wave per SIMD), so
+//     every uniformly routed DeepSeek-V3 expert (128 +- 11 rows) is one pass
+//     and its weights are read exactly once; longer segments take more
+//     passes, which are ordered side by side so they share the weight stream
+//     through L2.
+//   * The K loop is compiled per count of active 32-row fragments, so the
+//     MFMA stream has no branches.
+//   * The epilogue stages each 32-row fragment through a wave-private LDS
+//     tile and stores whole 16-byte runs of output rows.
+//
+// Packed layout (element = bf16, 8 per 16-byte lane chunk), per expert:
+//   GEMM1: [I/128 tiles][K/64 steps][4 waves][4 kk][2 j][64 lanes][8]
+//          tile t, wave w owns h columns c = t*128 + w*32 + (lane & 31);
+//          j = 0 holds w_gate row c, j = 1 holds w_up row c.
+//   GEMM2: [d/256 tiles][I/64 steps][4 waves][4 kk][2 j][64 lanes][8]
+//          wave w owns output columns t*256 + w*64 + j*32 + (lane & 31).
+//   The 8 elements of (step s, kk, lane) are k = s*64 + kk*16 + 8*(lane>>5) + 0..7.
+#include "moe_internal.h"
+
+#include <mutex>
+#include <type_traits>
+#include <utility>
+
+namespace moe {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxRows = 192;      // rows per pass
+constexpr int kStepBytes = 8192;   // one wave's weights per K step
+constexpr int kDepth = 4;          // weight register sets: the current K step and kDepth-1 in flight
+constexpr int kSlots = 2;          // A ring slots in LDS: the current step and the next
+constexpr int kUnroll = (kDepth % kSlots == 0) ? kDepth : kDepth * kSlots;  // K-loop unroll
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ __forceinline__ int lds_off(int row, int chunk) { return (row << 7) + ((chunk ^ (row & 7)) << 4); }
+__device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int N, typename F>
+__device__ __forceinline__ void with_count(int n, F&& f) {
+  if constexpr (N == 0) {
+    f(std::integral_constant<int, 0>{});
+  } else {
+    if (n == N) f(std::integral_constant<int, N>{});
+    else with_count<N - 1>(n, f);
+  }
+}
+
+__device__ int scan4(int v, int* scratch, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int n = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += n;
+  }
+  if (lane == 63) scratch[wave] = inc;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int s = scratch[w];
+    if (w < wave) base += s;
+    tot += s;
+  }
+  *total = tot;
+  return base + inc - v;
+}
+
+// EPI_SWIGLU: GEMM1 (j = gate/up, 32 output columns per wave);
+// EPI_STORE:  GEMM2 (j = two 32-column halves, 64 output columns per wave).
+template <int EPI>
+__global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
+  constexpr int WCOLS = (EPI == EPI_SWIGLU) ? 32 : 64;  // output columns per wave
+  constexpr int TCOLS = WCOLS * kWaves;                  // per tile
+  // Dynamic LDS: the A ring (kSlots slots of kMaxRows x 128 bytes), then one
+  // 32-row output staging tile per wave.
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ int tstart[257];
+  __shared__ int scan_scratch[kWaves];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int groups = p.offsets ? p.groups : 1;
+  {
+    int mt = 0;
+    if (tid < groups) {
+      int c = p.M;
+      if (p.offsets) {
+        const int lo = min(max(p.offsets[tid], 0), p.M);
+        c = min(max(p.offsets[tid + 1], lo), p.M) - lo;
+      }
+      mt = (c + kMaxRows - 1) / kMaxRows;
+    }
+    int total;
+    const int ex = scan4(mt, scan_scratch, &total);
+    if (tid < groups) tstart[tid] = ex;
+    if (tid == 0) tstart[groups] = total;
+    __syncthreads();
+  }
+  const int Nt = p.N / TCOLS;
+  const int total_tiles = tstart[groups] * Nt;
+  const int nk = p.K / 64;
+  const int G = gridDim.x, b = blockIdx.x;
+  const int vb = (G % 8 == 0) ? (b % 8) * (G / 8) + (b / 8) : b;
+  const uint32_t a_bytes = (uint32_t)((size_t)p.a_rows * p.K * 2);
+  const __amdgpu_buffer_rsrc_t a_rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.A), (short)0, (int)a_bytes, 0x00020000);
+  const int K = p.K;
+  // A rows move in 1 KB blocks of 8 rows: lane l carries row l/8, logical
+  // 16-byte chunk (l%8) ^ (l/8), stored at physical chunk l%8 (the XOR
+  // swizzle that lds_off() reads back).
+  const int lr = lane >> 3, lc = (lane & 7) ^ lr;
+
+  for (int tile = vb; tile < total_tiles; tile += G) {
+    // ---- decode: expert e, pass, column tile nt (passes of one tile side by side)
+    const int q = tile / Nt;
+    int lo = 0, hi = groups - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (tstart[mid] <= q) lo = mid; else hi = mid - 1;
+    }
+    const int e = lo;
+    const int local = tile - tstart[e] * Nt;
+    const int passes = tstart[e + 1] - tstart[e];
+    const int pass = local % passes;
+    const int nt = local / passes;
+    const int gbeg = p.offsets ? min(max(p.offsets[e], 0), p.M) : 0;
+    const int gend = p.offsets ? min(max(p.offsets[e + 1], gbeg), p.M) : p.M;
+    const int row0 = gbeg + pass * kMaxRows;
+    const int rows = min(kMaxRows, gend - row0);
+
+    // this wave's packed weights: contiguous nk * 32 KB per tile, 8 KB per wave per step
+    const char* bw = static_cast<const char*>(p.B0) +
+                     (((size_t)e * Nt + nt) * nk * kWaves + wave) * (size_t)kStepBytes + lane * 16;
+
+    f32x16 acc[kMaxRows / 32][2];
+#pragma unroll
+    for (int i = 0; i < kMaxRows / 32; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    const int nact = __builtin_amdgcn_readfirstlane((rows + 31) / 32);
+
+    auto body = [&](auto ar_c) {
+      constexpr int AR = decltype(ar_c)::value;  // A rows staged per step (128 or kMaxRows)
+      constexpr int A_CH = AR / (8 * kWaves);
+      constexpr int LOADS = A_CH + 8;
+      uint32_t a_off[A_CH];  // byte offsets into A (its size is checked below 4 GiB at launch)
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) {
+        const int r = min(i * 8 * kWaves + wave * 8 + lr, rows - 1);
+        const int ar = p.gather ? min(max(p.gather[row0 + r], 0), p.a_rows - 1) : row0 + r;
+        a_off[i] = (uint32_t)ar * (uint32_t)(K * 2) + lc * 16;
+      }
+      // Registers per in-flight K step: this wave's weights (kDepth sets: a
+      // step's weights are loaded kDepth-1 steps ahead) and its share of the next
+      // step's A rows (one set: loaded one step ahead, written to the LDS
+      // ring at the end of the step). Every load returns to registers, so the
+      // compiler's own wait counts (in-order returns) are exact and no
+      // hand-written vmcnt wait is needed.
+      i32x4 bq[kDepth][8];
+      i32x4 sa[A_CH];
+      // Steps past the end are clamped to the last one: those surplus loads
+      // are never used, which keeps the steady-state loop free of branches.
+      auto load_a = [&](int ks, int i) {
+        const int kc = min(ks, nk - 1);
+        sa[i] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, (int)(a_off[i] + kc * 128), 0, 0);
+      };
+      auto load_b = [&](int ks, auto s_c, int n) {
+        constexpr int S = decltype(s_c)::value;
+        const int kc = min(ks, nk - 1);
+        bq[S][n] = __builtin_nontemporal_load(
+            reinterpret_cast<const i32x4*>(bw + (size_t)kc * kWaves * kStepBytes + n * 1024));
+      };
+      // Write the staged A rows into ring slot S (row-major 128-byte rows,
+      // 16-byte chunks XOR-swizzled by row: lane l holds row l/8, chunk l%8).
+      auto stage = [&](auto s_c) {
+        constexpr int S = decltype(s_c)::value;
+        char* const dst = smem + S * (kMaxRows * 128) + wave * 8 * 128 + lane * 16;
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<i32x4*>(dst + i * 8 * kWaves * 128) = sa[i];
+      };
+
+      auto kloop = [&](auto nact_c) {
+        constexpr int NACT = decltype(nact_c)::value;
+        // Step ks (U = ks % kUnroll) multiplies with weight set U % kDepth and
+        // ring slot U % kSlots, loads step ks+1's A rows and step
+        // ks+kDepth-1's weights and, at its end, writes the A rows into the
+        // other ring slot, whose previous reader (step ks-1) left it before the
+        // barrier of step ks.
+        auto step = [&](int ks, auto u_c) {
+          constexpr int U = decltype(u_c)::value;
+          constexpr int BS = U % kDepth;
+          constexpr auto S1 = std::integral_constant<int, (U + 1) % kSlots>{};
+          constexpr auto SB = std::integral_constant<int, (U + kDepth - 1) % kDepth>{};
+          lds_barrier();  // slot U written by every wave
+          __builtin_amdgcn_sched_barrier(0);
+          if constexpr (NACT > 0) {
+            // Fixed instruction order (each group closed by a scheduling
+            // barrier): the first 16-wide K slice of A, then per row fragment
+            // the two MFMAs of one slice, the read of the same fragment's next
+            // slice (NACT groups to land) and an even share of this step's
+            // loads (A rows first). Spreading the loads keeps a load that
+            // waits for queue space from idling the matrix core for long.
+            const char* as = smem + (U % kSlots) * (kMaxRows * 128);
+            auto rd = [&](int kk, int i) {
+              return *reinterpret_cast<const i32x4*>(as + lds_off(32 * i + (lane & 31), 2 * kk + (lane >> 5)));
+            };
+            i32x4 af[NACT];
+#pragma unroll
+            for (int i = 0; i < NACT; ++i) af[i] = rd(0, i);
+            __builtin_amdgcn_sched_barrier(0);
+            constexpr int GROUPS = 4 * NACT;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+#pragma unroll
+              for (int i = 0; i < NACT; ++i) {
+                const int g = kk * NACT + i;
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[i]),
+                                                                      __builtin_bit_cast(bf16x8, bq[BS][kk * 2 + j]),
+                                                                      acc[i][j], 0, 0, 0);
+                if (kk < 3) af[i] = rd(kk + 1, i);
+#pragma unroll
+                for (int n = g * LOADS / GROUPS; n < (g + 1) * LOADS / GROUPS; ++n) {
+                  if (n < A_CH) load_a(ks + 1, n);
+                  else load_b(ks + kDepth - 1, SB, n - A_CH);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < A_CH; ++i) load_a(ks + 1, i);
+#pragma unroll
+            for (int n = 0; n < 8; ++n) load_b(ks + kDepth - 1, SB, n);
+          }
+          stage(S1);
+        };
+        lds_barrier();  // every wave is done with the previous tile's ring
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i) load_a(0, i);
+        static_for<kDepth - 1>([&](auto s_c) {
+#pragma unroll
+          for (int n = 0; n < 8; ++n) load_b(decltype(s_c)::value, s_c, n);
+        });
+        stage(std::integral_constant<int, 0>{});
+        int ks = 0;
+        for (; ks + kUnroll <= nk; ks += kUnroll) static_for<kUnroll>([&](auto u_c) { step(ks + u_c, u_c); });
+        static_for<kUnroll - 1>([&](auto u_c) {
+          if (ks + u_c < nk) step(ks + u_c, u_c);
+        });
+      };
+      with_count<AR / 32>(min(nact, AR / 32), kloop);
+    };
+    if (rows <= 128) body(std::integral_constant<int, 128>{});
+    else body(std::integral_constant<int, kMaxRows>{});
+
+    // ---- epilogue: one 32-row fragment at a time through a wave-private LDS
+    // tile, so each lane stores whole 16-byte runs of an output row.
+    char* const stg = smem + kSlots * kMaxRows * 128 + wave * (32 * WCOLS * 2);
+    __bf16* const C = static_cast<__bf16*>(p.C);
+    const size_t ldc = (size_t)p.ldc;
+    const int colbase = nt * TCOLS + wave * WCOLS;
+    constexpr int RCH = WCOLS / 8;  // 16-byte chunks per staged row
+#pragma unroll
+    for (int i = 0; i < kMaxRows / 32; ++i) {
+      if (i >= nact) break;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        __bf16* const srow = reinterpret_cast<__bf16*>(stg) + row * WCOLS + (lane & 31);
+        if (EPI == EPI_SWIGLU) {
+          srow[0] = static_cast<__bf16>(silu_f(acc[i][0][r]) * acc[i][1][r]);
+        } else {
+          srow[0] = static_cast<__bf16>(acc[i][0][r]);
+          srow[32] = static_cast<__bf16>(acc[i][1][r]);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 32 * RCH / 64; ++t) {
+        const int q = lane + 64 * t, row = q / RCH, cc = q % RCH;
+        const i32x4 v = *reinterpret_cast<const i32x4*>(stg + row * (WCOLS * 2) + cc * 16);
+        const int orow = 32 * i + row;
+        if (orow < rows) *reinterpret_cast<i32x4*>(C + (size_t)(row0 + orow) * ldc + colbase + cc * 8) = v;
+      }
+    }
+  }
+}
+
+// One 16-byte chunk per thread: packed position -> source row and k.
+__global__ void pack_kernel(const __bf16* __restrict__ w0, const __bf16* __restrict__ w1, __bf16* __restrict__ dst,
+                            int E, int N, int K, int gate_up) {
+  const int tcols = gate_up ? 128 : 256;
+  const int nt_all = N / tcols, nk = K / 64;
+  const size_t chunks_per_expert = (size_t)N * K / 8 * (gate_up ? 2 : 1);
+  const size_t total = chunks_per_expert * E;
+  for (size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x; c < total; c += (size_t)gridDim.x * blockDim.x) {
+    size_t r = c;
+    const int lane = (int)(r % 64); r /= 64;
+    const int j = (int)(r % 2); r /= 2;
+    const int kk = (int)(r % 4); r /= 4;
+    const int w = (int)(r % 4); r /= 4;
+    const int s = (int)(r % nk); r /= nk;
+    const int nt = (int)(r % nt_all); r /= nt_all;
+    const int e = (int)r;
+    const int k0 = s * 64 + kk * 16 + 8 * (lane >> 5);
+    const __bf16* src;
+    int row;
+    if (gate_up) {
+      row = nt * 128 + w * 32 + (lane & 31);
+      src = j ? w1 : w0;
+    } else {
+      row = nt * 256 + w * 64 + j * 32 + (lane & 31);
+      src = w0;
+    }
+    const i32x4 v = *reinterpret_cast<const i32x4*>(src + ((size_t)e * N + row) * K + k0);
+    *reinterpret_cast<i32x4*>(dst + c * 8) = v;
+  }
+}
+
+template <int EPI>
+hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
+  auto kern = gemm_stream_kernel<EPI>;
+  constexpr size_t lds = (size_t)kSlots * kMaxRows * 128 + kWaves * 32 * ((EPI == EPI_SWIGLU) ? 32 : 64) * 2;
+  static std::once_flag once;
+  static hipError_t init_err = hipSuccess;
+  std::call_once(once, [&] {
+    init_err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  });
+  if (init_err != hipSuccess) return init_err;
+  // A is addressed through a buffer resource: 32-bit byte offsets.
+  if ((size_t)p.a_rows * (size_t)p.K * 2 > 0xFFFFFFFFull) return hipErrorInvalidValue;
+  const int tcols = (EPI == EPI_SWIGLU) ? 128 : 256;
+  const int groups = p.offsets ? p.groups : 1;
+  const long long passes_upper = (p.M + kMaxRows - 1) / kMaxRows + (p.offsets ? groups : 0);
+  const long long upper = passes_upper * (p.N / tcols);
+  if (upper <= 0) return hipSuccess;
+  long long grid = device_cu_count();
+  if (grid > upper) grid = upper;
+  if (grid >= 8) grid -= grid % 8;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU>(p, s);
+  return launch_stream<EPI_STORE>(p, s);
+}
+
+hipError_t launch_pack(const void* w0, const void* w1, void* dst, int E, int N, int K, bool gate_up, hipStream_t s) {
+  const size_t chunks = (size_t)E * N * K / 8 * (gate_up ? 2 : 1);
+  if (chunks == 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<size_t>((chunks + 255) / 256, (size_t)device_cu_count() * 16);
+  hipLaunchKernelGGL(pack_kernel, dim3(grid), dim3(256), 0, s, static_cast<const __bf16*>(w0),
+                     static_cast<const __bf16*>(w1), static_cast<__bf16*>(dst), E, N, K, gate_up ? 1 : 0);
+  return hipGetLastError();
+}
+
+}  // namespace moe

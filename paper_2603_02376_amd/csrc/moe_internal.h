@@ -55,6 +55,12 @@ struct GemmProblem {
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
 // only); otherwise outputs are bf16.
 hipError_t launch_gemm_bf16(const GemmProblem& p, int epilogue, bool out_f32, hipStream_t s);
+// Weight-streaming bf16 grouped GEMM over packed weights (B0 = packed buffer;
+// N % 128 == 0 for EPI_SWIGLU, N % 256 == 0 for EPI_STORE, K % 64 == 0).
+hipError_t launch_gemm_stream(const GemmProblem& p, int epilogue, hipStream_t s);
+// Packs [E][N][K] row-major weights (gate_up: w0 = gate, w1 = up) into the
+// streaming kernel's layout.
+hipError_t launch_pack(const void* w0, const void* w1, void* dst, int E, int N, int K, bool gate_up, hipStream_t s);
 // fp32 grouped GEMM (vector ALU), same semantics, fp32 in and out.
 hipError_t launch_gemm_f32(const GemmProblem& p, int epilogue, hipStream_t s);
 

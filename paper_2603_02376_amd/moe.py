@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_PKG, "libmoe.so")
 
 MOE_F32, MOE_BF16 = 0, 1
 MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
+MOE_LAYOUT_ROWMAJOR, MOE_LAYOUT_PACKED = 0, 1
 STATUS = {0: "MOE_OK", -1: "MOE_ERR_INVALID_ARG", -2: "MOE_ERR_UNSUPPORTED",
           -3: "MOE_ERR_WORKSPACE", -4: "MOE_ERR_HIP"}
 
@@ -34,7 +35,8 @@ class moe_config_t(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("E", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("n_groups", ctypes.c_int32), ("topk_groups", ctypes.c_int32), ("I", ctypes.c_int32),
                 ("n_shared", ctypes.c_int32), ("I_shared", ctypes.c_int32), ("score", ctypes.c_int32),
-                ("renorm", ctypes.c_int32), ("route_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("renorm", ctypes.c_int32), ("route_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("weight_layout", ctypes.c_int32)]
 
 
 class moe_layer_debug_t(ctypes.Structure):
@@ -54,6 +56,7 @@ _SIGS = {
     "moe_combine": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
     "moe_layer": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ,
                                  _VP, _VP, ctypes.POINTER(moe_layer_debug_t)]),
+    "moe_pack_weights": (ctypes.c_int, [_CFG, _VP, _VP, _VP, _VP, _VP, _VP]),
     "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "moe_last_error": (ctypes.c_char_p, []),
     "moe_version": (ctypes.c_char_p, []),
@@ -101,6 +104,7 @@ class MoeConfig:
     renorm: bool = True
     scale: float = 1.0
     dtype: str = "bf16"        # "bf16" | "f32"
+    weight_layout: str = "rowmajor"  # "rowmajor" | "packed" (routed-expert weights, see moe_pack_weights)
 
     @property
     def torch_dtype(self):
@@ -110,7 +114,12 @@ class MoeConfig:
         return moe_config_t(self.d, self.E, self.k, self.n_groups, self.topk_groups, self.I, self.n_shared,
                             self.I_shared, MOE_SCORE_SIGMOID if self.score == "sigmoid" else MOE_SCORE_SOFTMAX,
                             int(bool(self.renorm)), float(self.scale),
-                            MOE_BF16 if self.dtype == "bf16" else MOE_F32)
+                            MOE_BF16 if self.dtype == "bf16" else MOE_F32,
+                            MOE_LAYOUT_PACKED if self.weight_layout == "packed" else MOE_LAYOUT_ROWMAJOR)
+
+    @property
+    def packed(self) -> bool:
+        return self.weight_layout == "packed"
 
 
 def workspace_size(cfg: MoeConfig, T: int) -> int:
@@ -189,10 +198,11 @@ def moe_expert_ffn(cfg: MoeConfig, T, x, sorted_token, offsets, w_gate, w_up, w_
     dt = cfg.torch_dtype
     n = T * cfg.k
     wsz = cfg.E * cfg.I * cfg.d
+    gsz = 2 * wsz if cfg.packed else wsz
     _check(lib().moe_expert_ffn(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
                                 _ptr(sorted_token, "sorted_token", torch.int32, n),
                                 _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
-                                _ptr(w_gate, "w_gate", dt, wsz), _ptr(w_up, "w_up", dt, wsz),
+                                _ptr(w_gate, "w_gate", dt, gsz), _ptr(w_up, "w_up", dt, wsz),
                                 _ptr(w_down, "w_down", dt, wsz), _ptr(y_perm, "y_perm", dt, n * cfg.d),
                                 _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
 
@@ -225,6 +235,7 @@ def moe_layer(cfg: MoeConfig, T, x, w_router, bias, w_gate, w_up, w_down, ws_gat
     c = cfg.c()
     dt = cfg.torch_dtype
     wsz = cfg.E * cfg.I * cfg.d
+    gsz = 2 * wsz if cfg.packed else wsz
     swsz = cfg.I_shared * cfg.d
     dbg_s = None
     if dbg:
@@ -234,12 +245,31 @@ def moe_layer(cfg: MoeConfig, T, x, w_router, bias, w_gate, w_up, w_down, ws_gat
         dbg_s = moe_layer_debug_t(**{k: _ptr(v, k) for k, v in dbg.items()})
     _check(lib().moe_layer(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
                            _ptr(w_router, "w_router", dt, cfg.E * cfg.d), _ptr(bias, "bias", torch.float32, cfg.E),
-                           _ptr(w_gate, "w_gate", dt, wsz), _ptr(w_up, "w_up", dt, wsz),
+                           _ptr(w_gate, "w_gate", dt, gsz), _ptr(w_up, "w_up", dt, wsz),
                            _ptr(w_down, "w_down", dt, wsz), _ptr(ws_gate, "ws_gate", dt, swsz),
                            _ptr(ws_up, "ws_up", dt, swsz), _ptr(ws_down, "ws_down", dt, swsz),
                            _ptr(out, "out", dt, T * cfg.d), _ptr(ws, "ws"), ws.numel() * ws.element_size(),
                            _stream(s_main), _stream(s_aux) if s_aux is not None else None,
                            ctypes.byref(dbg_s) if dbg_s is not None else None))
+
+
+def moe_pack_weights(cfg: MoeConfig, w_gate, w_up, w_down, gate_up_packed, down_packed, stream=None):
+    """Pack row-major routed-expert weights for MOE_LAYOUT_PACKED (either output may be None)."""
+    c = cfg.c()
+    wsz = cfg.E * cfg.I * cfg.d
+    _check(lib().moe_pack_weights(ctypes.byref(c), _ptr(w_gate, "w_gate", torch.bfloat16, wsz),
+                                  _ptr(w_up, "w_up", torch.bfloat16, wsz),
+                                  _ptr(w_down, "w_down", torch.bfloat16, wsz),
+                                  _ptr(gate_up_packed, "gate_up_packed", torch.bfloat16, 2 * wsz),
+                                  _ptr(down_packed, "down_packed", torch.bfloat16, wsz), _stream(stream)))
+
+
+def pack_weights(cfg: MoeConfig, w_gate, w_up, w_down):
+    """Allocate and fill the packed buffers; returns (gate_up_packed, down_packed)."""
+    gu = torch.empty(2 * w_gate.numel(), dtype=torch.bfloat16, device=w_gate.device)
+    dn = torch.empty(w_down.numel(), dtype=torch.bfloat16, device=w_down.device)
+    moe_pack_weights(cfg, w_gate, w_up, w_down, gu, dn)
+    return gu, dn
 
 
 def version() -> str:

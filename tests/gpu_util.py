@@ -32,7 +32,7 @@ def moe_cfg(p: dict) -> moe.MoeConfig:
     return moe.MoeConfig(d=p["d"], E=p["E"], k=p["k"], I=p["I"], n_groups=p.get("n_groups", 1),
                          topk_groups=p.get("topk_groups", 1), n_shared=p.get("n_shared", 0),
                          I_shared=p.get("I_shared", 0), score=p["score"], renorm=p.get("renorm", True),
-                         scale=p.get("scale", 1.0), dtype=p["dtype"])
+                         scale=p.get("scale", 1.0), dtype=p["dtype"], weight_layout=p.get("weight_layout", "rowmajor"))
 
 
 def oracle_cfg(p: dict) -> dict:
@@ -103,7 +103,11 @@ def run_layer(p: dict, t: dict, s_main=None, s_aux="new", with_debug=True) -> di
             dbg["shared_out"] = torch.empty((T, d), dtype=dt, device=dev)
     if s_aux == "new":
         s_aux = torch.cuda.Stream()
-    moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], t["w_gate"], t["w_up"], t["w_down"],
+    wg, wu, wd = t["w_gate"], t["w_up"], t["w_down"]
+    if cfg.packed:
+        wg, wd = moe.pack_weights(cfg, wg, wu, wd)
+        wu = None
+    moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], wg, wu, wd,
                   t["ws_gate"], t["ws_up"], t["ws_down"], out, ws, s_main=s_main, s_aux=s_aux, dbg=dbg)
     torch.cuda.synchronize()
     res = dict(out=out)

@@ -70,6 +70,9 @@ def test_workspace_size_presets(name):
     (dict(I=100), -2),                                  # I % 64
     (dict(n_shared=2, I_shared=64), -2),                # n_shared > 1
     (dict(n_shared=1, I_shared=0), -1),
+    (dict(weight_layout="packed"), -2),                 # packed needs d % 256 == 0
+    (dict(d=256, I=192, weight_layout="packed"), -2),   # and I % 128 == 0
+    (dict(d=256, I=128, dtype="f32", weight_layout="packed"), -2),
 ])
 def test_invalid_configs_rejected(kw, status):
     cfg = _cfg(**kw)
@@ -78,6 +81,17 @@ def test_invalid_configs_rejected(kw, status):
     r = moe.lib().moe_route(ctypes.byref(c), 16, None, None, None, FAKE, FAKE, FAKE, None, 0, None)
     assert r == status
     assert moe.lib().moe_last_error().decode()
+
+
+def test_packed_layout_rejects_operands_beyond_32bit_offsets():
+    cfg = _cfg(d=256, I=128, weight_layout="packed")
+    c = cfg.c()
+    assert moe.workspace_size(cfg, 1 << 16) > 0
+    big = 1 << 24                                       # T*d*2 bytes = 8 GiB
+    assert moe.workspace_size(cfg, big) == 0
+    r = moe.lib().moe_route(ctypes.byref(c), big, None, None, None, FAKE, FAKE, FAKE, None, 0, None)
+    assert r == -2
+    assert b"2^31" in moe.lib().moe_last_error()
 
 
 def test_null_and_negative_arguments():
@@ -112,6 +126,16 @@ def test_workspace_too_small_and_misaligned():
     assert b"workspace too small" in L.moe_last_error()
     assert L.moe_dispatch(*args, FAKE + 16, need, None) == -1
     assert L.moe_dispatch(*args, None, need, None) == -1
+
+
+def test_pack_weights_validation():
+    L = moe.lib()
+    c = _cfg(d=256, I=128).c()
+    assert L.moe_pack_weights(None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert L.moe_pack_weights(ctypes.byref(c), FAKE, None, FAKE, FAKE, FAKE, None) == -1   # w_up missing
+    assert L.moe_pack_weights(ctypes.byref(c), FAKE, FAKE, FAKE, None, None, None) == 0    # nothing to pack
+    bad = _cfg(d=128, I=128).c()
+    assert L.moe_pack_weights(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, None) == -2
 
 
 def test_zero_tokens_is_a_noop():

@@ -222,3 +222,68 @@ def test_combine(T, d, k, dtype, shared):
     want = O.combine(inputs.oracle_view(y), perm, w, inputs.oracle_view(sh))
     tol = 8e-3 if dtype == "bf16" else F32_TOL   # one bf16 rounding of the output
     assert max_rel_err(host(out.float()), want) <= tol
+
+
+# ---------------------------------------------------------------------------
+# packed weights and the weight-streaming expert GEMMs
+# ---------------------------------------------------------------------------
+
+def _unpack_reference(packed, E, N, K, gate_up):
+    """Row-major weights rebuilt from the packed buffer with plain reshapes,
+    following the layout documented in include/moe.h."""
+    nt = N // (128 if gate_up else 256)
+    v = packed.view(E, nt, K // 64, 4, 4, 2, 2, 32, 8)  # [e][t][s][w][kk][j][lane>>5][lane&31][8]
+    if gate_up:
+        # column = t*128 + w*32 + lane%32 (of gate for j = 0, up for j = 1); k = s*64 + kk*16 + (lane>>5)*8 + i
+        v = v.permute(5, 0, 1, 3, 7, 2, 4, 6, 8)            # [j][e][t][w][c][s][kk][half][8]
+        v = v.reshape(2, E, N, K)
+        return v[0], v[1]
+    v = v.permute(0, 1, 3, 5, 7, 2, 4, 6, 8)                 # [e][t][w][j][c][s][kk][half][8]
+    return v.reshape(E, N, K)
+
+
+@pytest.mark.parametrize("E,I,d", [(2, 128, 256), (3, 256, 512), (1, 2048, 7168)])
+def test_pack_weights_layout(E, I, d):
+    log("pack", E, I, d)
+    g = torch.Generator(device="cuda").manual_seed(E * 7 + I)
+    wg = torch.randn((E, I, d), generator=g, device="cuda").to(torch.bfloat16)
+    wu = torch.randn((E, I, d), generator=g, device="cuda").to(torch.bfloat16)
+    wd = torch.randn((E, d, I), generator=g, device="cuda").to(torch.bfloat16)
+    cfg = moe.MoeConfig(d=d, E=E, k=1, I=I, dtype="bf16", weight_layout="packed")
+    gu, dn = moe.pack_weights(cfg, wg, wu, wd)
+    torch.cuda.synchronize()
+    rg, ru = _unpack_reference(gu, E, I, d, True)
+    assert torch.equal(rg, wg) and torch.equal(ru, wu)
+    assert torch.equal(_unpack_reference(dn, E, d, I, False), wd)
+
+
+PACKED_CASES = [
+    # T, d, E, k, I, hot
+    (300, 256, 16, 4, 128, None),      # ~75 rows per expert: 128-row passes
+    (200, 512, 8, 4, 256, 0),          # one expert with 200 rows: two passes (192 + 8)
+    (1, 256, 8, 2, 128, None),
+    (64, 256, 64, 8, 128, None),       # ~8 rows per expert, some experts empty
+    (700, 256, 4, 2, 128, None),       # 350 rows per expert: 192 + 158
+    (513, 768, 32, 8, 384, None),
+]
+
+
+@pytest.mark.parametrize("case", PACKED_CASES, ids=lambda c: "T{}_d{}_E{}_k{}_I{}".format(*c[:5]))
+def test_expert_ffn_packed(case):
+    T, d, E, k, I, hot = case
+    log("expert_ffn packed", case)
+    p, t, idx = _ffn_inputs(T, d, E, k, I, "bf16", hot)
+    counts, offsets, st, sa, inv = O.dispatch(idx, E)
+    cfg = moe.MoeConfig(d=d, E=E, k=k, I=I, dtype="bf16", weight_layout="packed")
+    gu, dn = moe.pack_weights(cfg, t["w_gate"], t["w_up"], t["w_down"])
+    ws = moe.alloc_workspace(cfg, T)
+    y = torch.full((T * k, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    moe.moe_expert_ffn(cfg, T, t["x"], _dev(st), _dev(offsets), gu, None, dn, y, ws)
+    torch.cuda.synchronize()
+    want = O.expert_ffn(inputs.oracle_view(t["x"]), st, offsets, inputs.ExpertView(t["w_gate"]),
+                        inputs.ExpertView(t["w_up"]), inputs.ExpertView(t["w_down"]))
+    got = host(y.float())
+    assert np.isfinite(got).all(), "rows left unwritten"
+    err = max_rel_err(got, want)
+    log("  max_rel_err", err)
+    assert err <= BF16_TOL

@@ -80,6 +80,20 @@ def test_layer_deterministic_across_runs_and_streams():
     assert torch.equal(a["out"], d["out"])
 
 
+@pytest.mark.parametrize("name", ["dsv3_like_bf16", "decode_like_bf16"])
+def test_layer_packed_matches_rowmajor(name):
+    p = dict(SMALL[name], d=512, I=256)   # packed weights need I % 128 == 0 and d % 256 == 0
+    t = G.device_inputs(p, seed=5)
+    ref = G.run_layer(p, t)
+    routing = G.check_routing_and_dispatch_exact(p, t, ref)
+    y, sh, out = _oracle_full(p, t, ref, routing)
+    r = G.run_layer(dict(p, weight_layout="packed"), t)
+    for key in ("logits", "topk_idx", "topk_w", "counts", "offsets", "sorted_token", "inv_perm"):
+        assert torch.equal(ref[key], r[key]), key
+    assert max_rel_err(G.host(r["y_perm"].float()), y) <= G.tol(p)
+    assert max_rel_err(G.host(r["out"].float()), out) <= G.tol(p)
+
+
 def test_layer_on_side_streams():
     p = SMALL["dsv3_like_bf16"]
     t = G.device_inputs(p, seed=4)
@@ -94,13 +108,15 @@ def test_layer_on_side_streams():
 # full workload sizes (sampled outputs)
 # ---------------------------------------------------------------------------
 
-FULL = ["dsv3", "dsv3_skew", "dsv3_decode", "mixtral"]
+FULL = ["dsv3", "dsv3_packed", "dsv3_skew", "dsv3_decode", "mixtral"]
 SAMPLE = 8
 
 
 @pytest.mark.parametrize("name", FULL)
 def test_layer_full_size_sampled(name):
-    p = inputs.preset(name)
+    p = inputs.preset(name.replace("_packed", ""))
+    if name.endswith("_packed"):
+        p["weight_layout"] = "packed"
     G.log("full-size layer", name)
     t = G.device_inputs(p, seed=0, cache_weights=True)
     r = G.run_layer(p, t)
