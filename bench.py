@@ -4,10 +4,14 @@
 
 A step is one moe_layer call (gate, route, dispatch, grouped expert FFN,
 shared expert on a second stream, combine) over the workload's T tokens, with
-inputs and weights already resident in HBM. Prints ONE JSON line: tokens/s of
-the layer, the roofline of the dominant kernel pair (the grouped expert FFN,
-timed with HIP events on its own stream), and the CPU oracle timed on a
-bounded sample of the same workload as a baseline.
+inputs and weights already resident in HBM. By default the routed-expert
+weights are converted once, before any timing, into the packed layout of
+moe_pack_weights (a load-time conversion, like reading a checkpoint); the
+weight-streaming expert GEMMs then read them. --layout rowmajor times the
+tiled GEMMs on the plain [E][I][d] weights instead. Prints ONE JSON line:
+tokens/s of the layer, the roofline of the dominant kernel pair (the grouped
+expert FFN, timed with HIP events on its own stream), and the CPU oracle
+timed on a bounded sample of the same workload as a baseline.
 """
 from __future__ import annotations
 
@@ -45,28 +49,33 @@ def algorithmic(p: dict, counts) -> dict:
                 layer_flops=layer_flops, bytes_per_expert=w_expert)
 
 
-def kernel_source_hash() -> str:
+GEMM_SOURCES = {"packed": ("gemm_stream.hip",), "rowmajor": ("gemm_bf16.hip",)}
+
+
+def kernel_source_hash(layout: str = "packed") -> str:
+    """Hash of the expert-GEMM kernel sources of a weight layout: a traffic
+    record taken on other sources is not reported."""
     h = hashlib.sha256()
-    for f in ("gemm_bf16.hip",):
+    for f in GEMM_SOURCES[layout]:
         with open(os.path.join(ROOT, "paper_2603_02376_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, layout: str):
     """HBM bytes per expert-FFN call from the rocprofv3 counter runs committed
     under profiles/, or None when absent or taken on another kernel source."""
-    path = os.path.join(ROOT, "profiles", f"traffic_expert_ffn_{workload}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_expert_ffn_{workload}_{layout}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("kernel_source_hash") != kernel_source_hash():
+    if rec.get("kernel_source_hash") != kernel_source_hash(layout):
         return None
     return rec.get("bytes_per_call")
 
 
 def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens: int = 64,
-                 ffn_only: bool = False):
+                 ffn_only: bool = False, layout: str = "packed"):
     import numpy as np
     import torch
 
@@ -75,18 +84,26 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
     p = inputs.preset(name)
     cfg = moe.MoeConfig(d=p["d"], E=p["E"], k=p["k"], I=p["I"], n_groups=p["n_groups"],
                         topk_groups=p["topk_groups"], n_shared=p["n_shared"], I_shared=p["I_shared"],
-                        score=p["score"], renorm=p["renorm"], scale=p["scale"], dtype=p["dtype"])
+                        score=p["score"], renorm=p["renorm"], scale=p["scale"], dtype=p["dtype"],
+                        weight_layout=layout)
     T = p["T"]
     log(f"[bench] {name}: generating inputs on device")
     t = inputs.make_inputs(p, 0, "cuda")
+    w_ffn = (t["w_gate"], t["w_up"], t["w_down"])
+    w_sh = (t["ws_gate"], t["ws_up"], t["ws_down"])
+    if cfg.packed:  # one-time load-time conversion, outside every timed region
+        gu, dn = moe.pack_weights(cfg, *w_ffn)
+        w_ffn = (gu, None, dn)
+        if p["n_shared"]:
+            sg, sd = moe.pack_shared_weights(cfg, *w_sh)
+            w_sh = (sg, None, sd)
     ws = moe.alloc_workspace(cfg, T)
     out = torch.empty((T, p["d"]), dtype=cfg.torch_dtype, device="cuda")
     s_main = torch.cuda.current_stream()
     s_aux = torch.cuda.Stream()
 
     def layer(dbg=None):
-        moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], t["w_gate"], t["w_up"], t["w_down"],
-                      t["ws_gate"], t["ws_up"], t["ws_down"], out, ws, s_main=s_main, s_aux=s_aux, dbg=dbg)
+        moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], *w_ffn, *w_sh, out, ws, s_main=s_main, s_aux=s_aux, dbg=dbg)
 
     # untimed call that exports the routing, for the algorithmic byte count
     dbg = dict(counts=torch.empty(p["E"], dtype=torch.int32, device="cuda"),
@@ -120,8 +137,7 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
     y = torch.empty((T * p["k"], p["d"]), dtype=cfg.torch_dtype, device="cuda")
 
     def ffn():
-        moe.moe_expert_ffn(cfg, T, t["x"], dbg["sorted_token"], dbg["offsets"], t["w_gate"], t["w_up"],
-                           t["w_down"], y, ws, stream=s_main)
+        moe.moe_expert_ffn(cfg, T, t["x"], dbg["sorted_token"], dbg["offsets"], *w_ffn, y, ws, stream=s_main)
 
     log(f"[bench] {name}: timing {steps} expert-FFN calls")
     for _ in range(max(2, warmup)):
@@ -146,7 +162,7 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
     if want_cpu:
         log(f"[bench] {name}: CPU oracle baseline on {cpu_tokens} tokens")
         res["cpu"] = cpu_baseline(p, t, cpu_tokens)
-    del t, ws, out, y
+    del t, ws, out, y, w_ffn, w_sh
     torch.cuda.empty_cache()
     return res
 
@@ -197,6 +213,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dsv3")
+    ap.add_argument("--layout", choices=("packed", "rowmajor"), default="packed",
+                    help="routed-expert weight layout (packed: converted once before timing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the mixtral and decode side measurements")
     ap.add_argument("--cpu-tokens", type=int, default=64, help="tokens in the CPU-oracle baseline sample")
@@ -229,7 +247,7 @@ def main():
         log(f"[bench] copy calibration: 3 x {n} B, {2 * 3 * n / (c0.elapsed_time(c1) / 1e3) / 1e9:.1f} GB/s")
         del src, dst
     main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_tokens,
-                            args.ffn_only)
+                            args.ffn_only, args.layout)
     if args.ffn_only:
         print(json.dumps(dict(workload=args.workload, expert_ffn_ms=main_res["ffn_ms"],
                               expert_ffn_gbs=main_res["ffn_gbs"], expert_ffn_tflops=main_res["ffn_tflops"])))
@@ -239,7 +257,7 @@ def main():
         for name in ("dsv3_decode", "mixtral"):
             if name == args.workload:
                 continue
-            r = run_workload(name, args.steps, args.warmup, False)
+            r = run_workload(name, args.steps, args.warmup, False, layout=args.layout)
             extra[name] = dict(tokens_per_s=round(r["tokens_per_s"], 1), ms_per_step=round(r["ms"], 4),
                                layer_hbm_frac=round(r["layer_hbm_frac"], 4),
                                layer_mfma_frac=round(r["layer_mfma_frac"], 4),
@@ -256,8 +274,10 @@ def main():
     else:
         roof = dict(bound="mfma", achieved=round(r["ffn_tflops"], 1), peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                     frac=round(r["ffn_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4))
-    roof["traffic"] = measured_traffic(args.workload)
-    roof.update(kernel="moe_expert_ffn: grouped GEMM1+SwiGLU and grouped GEMM2 (2 launches per call)",
+    roof["traffic"] = measured_traffic(args.workload, args.layout)
+    kern = ("weight-streaming GEMM1+SwiGLU and GEMM2 over packed weights" if args.layout == "packed"
+            else "tiled grouped GEMM1+SwiGLU and GEMM2 over row-major weights")
+    roof.update(kernel=f"moe_expert_ffn: {kern} (2 launches per call)",
                 ms_per_call=round(r["ffn_ms"], 4), algorithmic_bytes=alg["ffn_bytes"],
                 algorithmic_flops=alg["ffn_flops"], touched_experts=alg["touched_experts"])
     out = {
@@ -275,7 +295,8 @@ def main():
         "data": "synthetic (seeded; random-init weights of the workload's shape)",
         "config": {"workload": (f"{args.workload}: T={p['T']} d={p['d']} E={p['E']} top-{p['k']}"
                                 + (f" (top-{p['topk_groups']} of {p['n_groups']} groups)" if p["n_groups"] > 1 else "")
-                                + f" I={p['I']}" + (f" + shared I={p['I_shared']}" if p["n_shared"] else "")),
+                                + f" I={p['I']}" + (f" + shared I={p['I_shared']}" if p["n_shared"] else "")
+                                + f", {args.layout} expert weights"),
                    "global_batch": p["T"], "parallelism": "single GPU (one GPU's share of expert parallelism)"},
         "layer_hbm_frac": round(r["layer_hbm_frac"], 4),
         "layer_mfma_frac": round(r["layer_mfma_frac"], 4),

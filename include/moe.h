@@ -73,7 +73,8 @@ typedef enum {
   MOE_SCORE_SIGMOID = 1  /* DeepSeek-V3: sigmoid scores, selection on s + bias  */
 } moe_score_t;
 
-/* Layout of the routed-expert weights passed to moe_expert_ffn / moe_layer. */
+/* Layout of the expert weights passed to moe_expert_ffn, moe_shared_ffn and
+ * moe_layer (routed and shared experts alike). */
 typedef enum {
   MOE_LAYOUT_ROWMAJOR = 0, /* w_gate, w_up [E][I][d]; w_down [E][d][I]                       */
   MOE_LAYOUT_PACKED = 1    /* from moe_pack_weights: w_gate = packed gate+up, w_up = NULL,
@@ -175,6 +176,10 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x,
 /*
  * moe_shared_ffn — the shared expert: the same SwiGLU FFN, with intermediate
  * size cfg->I_shared, applied to all T tokens (dense, unweighted).
+ *  ws_gate, ws_up, ws_down : row-major, or with MOE_LAYOUT_PACKED the output
+ *        of moe_pack_weights for the shared expert alone (a config with E = 1
+ *        and I = I_shared): ws_gate = packed gate+up, ws_up = NULL,
+ *        ws_down = packed down.
  *  out : [T][d] dtype out. Requires cfg->n_shared == 1.
  */
 int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void* ws_gate,
@@ -199,7 +204,12 @@ int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const in
  * (the single-GPU form of the paper's two-stream overlap, §4.3: dispatch on
  * one stream concurrent with expert compute on another, joined by an event).
  *  s_aux  : may be NULL or equal to s_main (then everything runs on s_main).
- *  ws_*   : shared-expert weights, required iff cfg->n_shared == 1.
+ *  ws_*   : shared-expert weights, required iff cfg->n_shared == 1, in the
+ *           layout of cfg->weight_layout (see moe_shared_ffn). With packed
+ *           weights and I_shared == I the shared expert is not run on s_aux:
+ *           it is computed inside the routed expert GEMMs as one more group
+ *           (its compute fills the matrix cores of the memory-bound routed
+ *           work); the result is the same.
  *  out    : [T][d] dtype out.
  *  dbg    : NULL, or device buffers to receive intermediates (see above).
  * On return, s_main carries all the work (s_aux is joined into it).

@@ -107,12 +107,14 @@ int validate(const moe_config_t* c, int32_t T) {
   if ((int64_t)T * c->k >= (int64_t)1 << 31) return fail(MOE_ERR_UNSUPPORTED, "T*k >= 2^31");
   if (c->weight_layout != MOE_LAYOUT_ROWMAJOR && c->weight_layout != MOE_LAYOUT_PACKED)
     return fail(MOE_ERR_INVALID_ARG, "unknown weight layout");
-  if (c->weight_layout == MOE_LAYOUT_PACKED && (c->dtype != MOE_BF16 || c->I % 128 != 0 || c->d % 256 != 0))
-    return fail(MOE_ERR_UNSUPPORTED, "packed weights need bf16, I % 128 == 0 and d % 256 == 0");
+  if (c->weight_layout == MOE_LAYOUT_PACKED &&
+      (c->dtype != MOE_BF16 || c->I % 128 != 0 || c->d % 256 != 0 || (c->n_shared && c->I_shared % 128 != 0)))
+    return fail(MOE_ERR_UNSUPPORTED, "packed weights need bf16, I and I_shared % 128 == 0 and d % 256 == 0");
   // The weight-streaming GEMMs address their row operand (x, then the
   // intermediate h) with 32-bit byte offsets.
   if (c->weight_layout == MOE_LAYOUT_PACKED &&
-      ((int64_t)T * c->d * 2 > (int64_t)UINT32_MAX || (int64_t)T * c->k * c->I * 2 > (int64_t)UINT32_MAX))
+      ((int64_t)T * c->d * 2 > (int64_t)UINT32_MAX || (int64_t)T * c->k * c->I * 2 > (int64_t)UINT32_MAX ||
+       (int64_t)T * c->n_shared * c->I_shared * 2 > (int64_t)UINT32_MAX))
     return fail(MOE_ERR_UNSUPPORTED, "packed weights need T*d and T*k*I below 2^31 elements");
   return MOE_OK;
 }
@@ -209,11 +211,22 @@ hipError_t run_dispatch(const moe_config_t& c, int32_t T, const int32_t* idx, ch
   return moe::launch_dispatch(d, s);
 }
 
+// The shared expert fused into the routed weight-streaming launches as one
+// extra group: its packed weights, its intermediate and output buffers.
+struct FusedShared {
+  const void* w_gate_up = nullptr;
+  const void* w_down = nullptr;
+  void* h = nullptr;
+  void* out = nullptr;
+};
+
 // Dense or grouped SwiGLU FFN: h = silu(X Wgᵀ) * (X Wuᵀ) into `h`, then
-// y = h Wdᵀ into `y`.
+// y = h Wdᵀ into `y`. packed: weights from moe_pack_weights (wu unused) and
+// the weight-streaming kernel; fused (packed only, same intermediate size):
+// the shared expert over all a_rows tokens rides along as an extra group.
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
-                   void* h, void* y, hipStream_t s, bool packed = false) {
+                   void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr) {
   moe::GemmProblem up{};
   up.A = x;
   up.a_rows = a_rows;
@@ -227,6 +240,12 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   up.K = c.d;
   up.C = h;
   up.ldc = inter;
+  if (fused) {
+    up.xA = x;
+    up.xB = fused->w_gate_up;
+    up.xC = fused->h;
+    up.x_rows = a_rows;
+  }
   hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
   if (e != hipSuccess) return e;
   moe::GemmProblem down{};
@@ -240,6 +259,12 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   down.K = inter;
   down.C = y;
   down.ldc = c.d;
+  if (fused) {
+    down.xA = fused->h;
+    down.xB = fused->w_down;
+    down.xC = fused->out;
+    down.x_rows = a_rows;
+  }
   return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
@@ -368,16 +393,17 @@ int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void
                    const void* ws_down, void* out, void* ws, size_t ws_bytes, hipStream_t stream) {
   MOE_CHECK(validate(cfg, T));
   if (cfg->n_shared != 1) return fail(MOE_ERR_INVALID_ARG, "config has no shared expert");
+  const bool packed = cfg->weight_layout == MOE_LAYOUT_PACKED;
   MOE_CHECK(need(x, "x"));
   MOE_CHECK(need(ws_gate, "ws_gate"));
-  MOE_CHECK(need(ws_up, "ws_up"));
+  if (!packed) MOE_CHECK(need(ws_up, "ws_up"));
   MOE_CHECK(need(ws_down, "ws_down"));
   MOE_CHECK(need(out, "out"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (T == 0) return MOE_OK;
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T, 1, cfg->I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down,
-                               static_cast<char*>(ws) + L.shared_h, out, stream);
+                               static_cast<char*>(ws) + L.shared_h, out, stream, packed);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "shared FFN");
 }
 
@@ -410,7 +436,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   MOE_CHECK(need(out, "out"));
   if (c.n_shared) {
     MOE_CHECK(need(ws_gate, "ws_gate"));
-    MOE_CHECK(need(ws_up, "ws_up"));
+    if (!packed) MOE_CHECK(need(ws_up, "ws_up"));
     MOE_CHECK(need(ws_down, "ws_down"));
   }
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
@@ -436,7 +462,12 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   void* shared = c.n_shared ? (d.shared_out ? d.shared_out : w + L.shared_out) : nullptr;
 
   hipError_t e;
-  const bool two = c.n_shared && s_aux && s_aux != s_main;
+  // Packed weights with equal intermediate sizes: the shared expert runs
+  // inside the routed expert GEMMs as one more group, so its compute fills
+  // the matrix cores of the memory-bound routed work. Otherwise it runs on
+  // its own, on s_aux when given (overlapping gate, routing and dispatch).
+  const bool fuse = packed && c.n_shared && c.I_shared == c.I;
+  const bool two = c.n_shared && !fuse && s_aux && s_aux != s_main;
   StreamEvents* ev = nullptr;
   if (two) {
     // fork: the shared expert on s_aux may start once x is ready on s_main
@@ -444,7 +475,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     if ((e = hipEventRecord(ev->fork, s_main)) != hipSuccess) return hip_fail(e, "event record");
     if ((e = hipStreamWaitEvent(s_aux, ev->fork, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h, shared,
-                     s_aux)) != hipSuccess)
+                     s_aux, packed)) != hipSuccess)
       return hip_fail(e, "shared FFN");
     if ((e = hipEventRecord(ev->join, s_aux)) != hipSuccess) return hip_fail(e, "event record");
   }
@@ -453,14 +484,21 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     return hip_fail(e, "route");
   if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main)) != hipSuccess)
     return hip_fail(e, "dispatch");
-  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main, packed)) !=
-      hipSuccess)
+  FusedShared fs;
+  if (fuse) {
+    fs.w_gate_up = ws_gate;
+    fs.w_down = ws_down;
+    fs.h = w + L.shared_h;
+    fs.out = shared;
+  }
+  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main, packed,
+                   fuse ? &fs : nullptr)) != hipSuccess)
     return hip_fail(e, "expert FFN");
-  if (c.n_shared) {
+  if (c.n_shared && !fuse) {
     if (two) {
       if ((e = hipStreamWaitEvent(s_main, ev->join, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     } else if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h,
-                            shared, s_main)) != hipSuccess) {
+                            shared, s_main, packed)) != hipSuccess) {
       return hip_fail(e, "shared FFN");
     }
   }

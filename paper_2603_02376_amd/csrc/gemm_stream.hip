@@ -62,7 +62,11 @@ constexpr int kUnroll = (kDepth % kSlots == 0) ? kDepth : kDepth * kSlots;  // K
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-__device__ __forceinline__ int lds_off(int row, int chunk) { return (row << 7) + ((chunk ^ (row & 7)) << 4); }
+// A ring layout: 128-byte rows of 8 16-byte chunks, chunk c of row r stored at
+// chunk c ^ ((r >> 1) & 7). The 16 rows one quarter-wave reads with a 16-byte
+// load (lanes 0-15 or 16-31 of a fragment) then fall on 16 distinct 16-byte
+// bank groups.
+__device__ __forceinline__ int lds_off(int row, int chunk) { return (row << 7) + ((chunk ^ ((row >> 1) & 7)) << 4); }
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 template <typename F, int... Is>
@@ -136,40 +140,83 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     __syncthreads();
   }
   const int Nt = p.N / TCOLS;
-  const int total_tiles = tstart[groups] * Nt;
+  // Work: Nt column tiles per pass (up to kMaxRows rows of one group). The
+  // tile sequence is Nt segments: a 1/Nt share of the routed tiles, then the
+  // extra group's passes of column tile j side by side (adjacent tiles run on
+  // one XCD at the same time and share that weight stream through its L2),
+  // so the extra group's compute-heavy full passes run next to memory-heavy
+  // routed ones rather than all at the end.
+  const int routed_tiles = tstart[groups] * Nt;
+  const int units_x = (p.x_rows + kMaxRows - 1) / kMaxRows;
+  const int total_tiles = routed_tiles + Nt * units_x;
+  auto seg_start = [&](int j) { return (int)((int64_t)j * routed_tiles / Nt) + j * units_x; };
   const int nk = p.K / 64;
   const int G = gridDim.x, b = blockIdx.x;
   const int vb = (G % 8 == 0) ? (b % 8) * (G / 8) + (b / 8) : b;
-  const uint32_t a_bytes = (uint32_t)((size_t)p.a_rows * p.K * 2);
-  const __amdgpu_buffer_rsrc_t a_rs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.A), (short)0, (int)a_bytes, 0x00020000);
   const int K = p.K;
-  // A rows move in 1 KB blocks of 8 rows: lane l carries row l/8, logical
-  // 16-byte chunk (l%8) ^ (l/8), stored at physical chunk l%8 (the XOR
-  // swizzle that lds_off() reads back).
-  const int lr = lane >> 3, lc = (lane & 7) ^ lr;
+  // A rows move in 1 KB blocks of 8 rows (block b of a wave: rows 32b + 8 wave
+  // + 0..7): lane l carries row l/8 of the block and the logical 16-byte chunk
+  // that lds_off() places at physical chunk l%8.
+  const int lr = lane >> 3, lc = (lane & 7) ^ ((wave * 4 + (lr >> 1)) & 7);
 
   for (int tile = vb; tile < total_tiles; tile += G) {
-    // ---- decode: expert e, pass, column tile nt (passes of one tile side by side)
-    const int q = tile / Nt;
-    int lo = 0, hi = groups - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (tstart[mid] <= q) lo = mid; else hi = mid - 1;
+    // ---- decode: group, pass and column tile nt
+    int seg = 0;
+    if (units_x > 0) {
+      int lo = 0, hi = Nt - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (seg_start(mid) <= tile) lo = mid; else hi = mid - 1;
+      }
+      seg = lo;
     }
-    const int e = lo;
-    const int local = tile - tstart[e] * Nt;
-    const int passes = tstart[e + 1] - tstart[e];
-    const int pass = local % passes;
-    const int nt = local / passes;
-    const int gbeg = p.offsets ? min(max(p.offsets[e], 0), p.M) : 0;
-    const int gend = p.offsets ? min(max(p.offsets[e + 1], gbeg), p.M) : p.M;
-    const int row0 = gbeg + pass * kMaxRows;
-    const int rows = min(kMaxRows, gend - row0);
+    const int r_beg = (int)((int64_t)seg * routed_tiles / Nt);
+    const int r_len = (int)((int64_t)(seg + 1) * routed_tiles / Nt) - r_beg;
+    const int off = units_x > 0 ? tile - seg_start(seg) : tile;
+    const bool extra = units_x > 0 && off >= r_len;  // pass off - r_len of the extra group, column tile seg
+    const void* a_base;
+    const int32_t* gather;
+    int a_rows, row0, rows, nt;
+    const char* b_base;
+    __bf16* c_base;
+    if (extra) {
+      a_base = p.xA;
+      a_rows = p.x_rows;
+      gather = nullptr;
+      nt = seg;
+      row0 = (off - r_len) * kMaxRows;
+      rows = min(kMaxRows, p.x_rows - row0);
+      b_base = static_cast<const char*>(p.xB) + (size_t)nt * nk * kWaves * kStepBytes;
+      c_base = static_cast<__bf16*>(p.xC);
+    } else {
+      // routed tile rt; an expert's passes of one column tile are side by side
+      const int rt = units_x > 0 ? r_beg + off : tile;
+      const int q = rt / Nt;
+      int lo = 0, hi = groups - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tstart[mid] <= q) lo = mid; else hi = mid - 1;
+      }
+      const int e = lo;
+      const int local = rt - tstart[e] * Nt;
+      const int passes = tstart[e + 1] - tstart[e];
+      const int pass = local % passes;
+      nt = local / passes;
+      const int gbeg = p.offsets ? min(max(p.offsets[e], 0), p.M) : 0;
+      const int gend = p.offsets ? min(max(p.offsets[e + 1], gbeg), p.M) : p.M;
+      a_base = p.A;
+      a_rows = p.a_rows;
+      gather = p.gather;
+      row0 = gbeg + pass * kMaxRows;
+      rows = min(kMaxRows, gend - row0);
+      b_base = static_cast<const char*>(p.B0) + ((size_t)e * Nt + nt) * nk * kWaves * kStepBytes;
+      c_base = static_cast<__bf16*>(p.C);
+    }
+    const __amdgpu_buffer_rsrc_t a_rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(a_base), (short)0, (int)(uint32_t)((size_t)a_rows * K * 2), 0x00020000);
 
     // this wave's packed weights: contiguous nk * 32 KB per tile, 8 KB per wave per step
-    const char* bw = static_cast<const char*>(p.B0) +
-                     (((size_t)e * Nt + nt) * nk * kWaves + wave) * (size_t)kStepBytes + lane * 16;
+    const char* bw = b_base + (size_t)wave * kStepBytes + lane * 16;
 
     f32x16 acc[kMaxRows / 32][2];
 #pragma unroll
@@ -188,7 +235,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
 #pragma unroll
       for (int i = 0; i < A_CH; ++i) {
         const int r = min(i * 8 * kWaves + wave * 8 + lr, rows - 1);
-        const int ar = p.gather ? min(max(p.gather[row0 + r], 0), p.a_rows - 1) : row0 + r;
+        const int ar = gather ? min(max(gather[row0 + r], 0), a_rows - 1) : row0 + r;
         a_off[i] = (uint32_t)ar * (uint32_t)(K * 2) + lc * 16;
       }
       // Registers per in-flight K step: this wave's weights (kDepth sets: a
@@ -211,8 +258,8 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         bq[S][n] = __builtin_nontemporal_load(
             reinterpret_cast<const i32x4*>(bw + (size_t)kc * kWaves * kStepBytes + n * 1024));
       };
-      // Write the staged A rows into ring slot S (row-major 128-byte rows,
-      // 16-byte chunks XOR-swizzled by row: lane l holds row l/8, chunk l%8).
+      // Write the staged A rows into ring slot S (layout of lds_off(): lane l
+      // holds row l/8 of each 8-row block, at physical chunk l%8).
       auto stage = [&](auto s_c) {
         constexpr int S = decltype(s_c)::value;
         char* const dst = smem + S * (kMaxRows * 128) + wave * 8 * 128 + lane * 16;
@@ -299,7 +346,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     // ---- epilogue: one 32-row fragment at a time through a wave-private LDS
     // tile, so each lane stores whole 16-byte runs of an output row.
     char* const stg = smem + kSlots * kMaxRows * 128 + wave * (32 * WCOLS * 2);
-    __bf16* const C = static_cast<__bf16*>(p.C);
+    __bf16* const C = c_base;
     const size_t ldc = (size_t)p.ldc;
     const int colbase = nt * TCOLS + wave * WCOLS;
     constexpr int RCH = WCOLS / 8;  // 16-byte chunks per staged row
@@ -370,10 +417,13 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
   });
   if (init_err != hipSuccess) return init_err;
   // A is addressed through a buffer resource: 32-bit byte offsets.
-  if ((size_t)p.a_rows * (size_t)p.K * 2 > 0xFFFFFFFFull) return hipErrorInvalidValue;
+  if ((size_t)p.a_rows * (size_t)p.K * 2 > 0xFFFFFFFFull || (size_t)p.x_rows * (size_t)p.K * 2 > 0xFFFFFFFFull)
+    return hipErrorInvalidValue;
+  if (p.x_rows < 0 || (p.x_rows > 0 && (!p.xA || !p.xB || !p.xC))) return hipErrorInvalidValue;
   const int tcols = (EPI == EPI_SWIGLU) ? 128 : 256;
   const int groups = p.offsets ? p.groups : 1;
-  const long long passes_upper = (p.M + kMaxRows - 1) / kMaxRows + (p.offsets ? groups : 0);
+  const long long passes_upper =
+      (p.M + kMaxRows - 1) / kMaxRows + (p.offsets ? groups : 0) + (p.x_rows + kMaxRows - 1) / kMaxRows;
   const long long upper = passes_upper * (p.N / tcols);
   if (upper <= 0) return hipSuccess;
   long long grid = device_cu_count();
@@ -386,7 +436,7 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
-  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  if ((p.M <= 0 && p.x_rows <= 0) || p.N <= 0) return hipSuccess;
   if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU>(p, s);
   return launch_stream<EPI_STORE>(p, s);
 }

@@ -50,6 +50,14 @@ struct GemmProblem {
   int32_t ksplit;
   int64_t c_split_stride;
   int32_t tile;  // GemmTile
+  // Weight-streaming kernel only: one extra group (the shared expert, fused
+  // into the routed launch) of x_rows rows of xA, taken in order (no gather),
+  // with packed weights xB (one expert, same N and K) and output rows in xC
+  // (leading dimension ldc). x_rows == 0: none.
+  const void* xA;
+  const void* xB;
+  void* xC;
+  int32_t x_rows;
 };
 
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE

@@ -10,6 +10,7 @@ there is no fallback.
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 import os
 from dataclasses import dataclass
 
@@ -104,7 +105,7 @@ class MoeConfig:
     renorm: bool = True
     scale: float = 1.0
     dtype: str = "bf16"        # "bf16" | "f32"
-    weight_layout: str = "rowmajor"  # "rowmajor" | "packed" (routed-expert weights, see moe_pack_weights)
+    weight_layout: str = "rowmajor"  # "rowmajor" | "packed" (expert weights, see moe_pack_weights)
 
     @property
     def torch_dtype(self):
@@ -211,8 +212,9 @@ def moe_shared_ffn(cfg: MoeConfig, T, x, ws_gate, ws_up, ws_down, out, ws, strea
     c = cfg.c()
     dt = cfg.torch_dtype
     wsz = cfg.I_shared * cfg.d
+    gsz = 2 * wsz if cfg.packed else wsz   # packed: gate and up in one buffer, ws_up None
     _check(lib().moe_shared_ffn(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
-                                _ptr(ws_gate, "ws_gate", dt, wsz), _ptr(ws_up, "ws_up", dt, wsz),
+                                _ptr(ws_gate, "ws_gate", dt, gsz), _ptr(ws_up, "ws_up", dt, wsz),
                                 _ptr(ws_down, "ws_down", dt, wsz), _ptr(out, "out", dt, T * cfg.d),
                                 _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
 
@@ -237,6 +239,7 @@ def moe_layer(cfg: MoeConfig, T, x, w_router, bias, w_gate, w_up, w_down, ws_gat
     wsz = cfg.E * cfg.I * cfg.d
     gsz = 2 * wsz if cfg.packed else wsz
     swsz = cfg.I_shared * cfg.d
+    sgsz = 2 * swsz if cfg.packed else swsz
     dbg_s = None
     if dbg:
         unknown = set(dbg) - {f for f, _ in moe_layer_debug_t._fields_}
@@ -246,7 +249,7 @@ def moe_layer(cfg: MoeConfig, T, x, w_router, bias, w_gate, w_up, w_down, ws_gat
     _check(lib().moe_layer(ctypes.byref(c), T, _ptr(x, "x", dt, T * cfg.d),
                            _ptr(w_router, "w_router", dt, cfg.E * cfg.d), _ptr(bias, "bias", torch.float32, cfg.E),
                            _ptr(w_gate, "w_gate", dt, gsz), _ptr(w_up, "w_up", dt, wsz),
-                           _ptr(w_down, "w_down", dt, wsz), _ptr(ws_gate, "ws_gate", dt, swsz),
+                           _ptr(w_down, "w_down", dt, wsz), _ptr(ws_gate, "ws_gate", dt, sgsz),
                            _ptr(ws_up, "ws_up", dt, swsz), _ptr(ws_down, "ws_down", dt, swsz),
                            _ptr(out, "out", dt, T * cfg.d), _ptr(ws, "ws"), ws.numel() * ws.element_size(),
                            _stream(s_main), _stream(s_aux) if s_aux is not None else None,
@@ -254,7 +257,7 @@ def moe_layer(cfg: MoeConfig, T, x, w_router, bias, w_gate, w_up, w_down, ws_gat
 
 
 def moe_pack_weights(cfg: MoeConfig, w_gate, w_up, w_down, gate_up_packed, down_packed, stream=None):
-    """Pack row-major routed-expert weights for MOE_LAYOUT_PACKED (either output may be None)."""
+    """Pack row-major expert weights for MOE_LAYOUT_PACKED (either output may be None)."""
     c = cfg.c()
     wsz = cfg.E * cfg.I * cfg.d
     _check(lib().moe_pack_weights(ctypes.byref(c), _ptr(w_gate, "w_gate", torch.bfloat16, wsz),
@@ -270,6 +273,13 @@ def pack_weights(cfg: MoeConfig, w_gate, w_up, w_down):
     dn = torch.empty(w_down.numel(), dtype=torch.bfloat16, device=w_down.device)
     moe_pack_weights(cfg, w_gate, w_up, w_down, gu, dn)
     return gu, dn
+
+
+def pack_shared_weights(cfg: MoeConfig, ws_gate, ws_up, ws_down):
+    """Packed buffers of the shared expert ([I_shared][d] and [d][I_shared]
+    weights, packed as a single expert); returns (gate_up_packed, down_packed)."""
+    one = dataclasses.replace(cfg, E=1, k=1, n_groups=1, topk_groups=1, I=cfg.I_shared, n_shared=0, I_shared=0)
+    return pack_weights(one, ws_gate.unsqueeze(0), ws_up.unsqueeze(0), ws_down.unsqueeze(0))
 
 
 def version() -> str:

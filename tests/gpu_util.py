@@ -104,11 +104,15 @@ def run_layer(p: dict, t: dict, s_main=None, s_aux="new", with_debug=True) -> di
     if s_aux == "new":
         s_aux = torch.cuda.Stream()
     wg, wu, wd = t["w_gate"], t["w_up"], t["w_down"]
+    sg, su, sd = t.get("ws_gate"), t.get("ws_up"), t.get("ws_down")
     if cfg.packed:
         wg, wd = moe.pack_weights(cfg, wg, wu, wd)
         wu = None
+        if p.get("n_shared", 0):
+            sg, sd = moe.pack_shared_weights(cfg, sg, su, sd)
+            su = None
     moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], wg, wu, wd,
-                  t["ws_gate"], t["ws_up"], t["ws_down"], out, ws, s_main=s_main, s_aux=s_aux, dbg=dbg)
+                  sg, su, sd, out, ws, s_main=s_main, s_aux=s_aux, dbg=dbg)
     torch.cuda.synchronize()
     res = dict(out=out)
     if dbg:

@@ -73,6 +73,7 @@ def test_workspace_size_presets(name):
     (dict(weight_layout="packed"), -2),                 # packed needs d % 256 == 0
     (dict(d=256, I=192, weight_layout="packed"), -2),   # and I % 128 == 0
     (dict(d=256, I=128, dtype="f32", weight_layout="packed"), -2),
+    (dict(d=256, I=128, n_shared=1, I_shared=192, weight_layout="packed"), -2),  # I_shared % 128
 ])
 def test_invalid_configs_rejected(kw, status):
     cfg = _cfg(**kw)

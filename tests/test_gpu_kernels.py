@@ -199,6 +199,24 @@ def test_shared_ffn(T, d, Is, dtype):
     assert max_rel_err(host(out.float()), want) <= (BF16_TOL if dtype == "bf16" else F32_TOL)
 
 
+@pytest.mark.parametrize("T,d,Is", [(300, 512, 256), (5, 256, 128), (700, 256, 384)])
+def test_shared_ffn_packed(T, d, Is):
+    log("shared_ffn packed", T, d, Is)
+    p = dict(T=T, d=d, E=1, k=1, I=128, dtype="bf16", n_shared=1, I_shared=Is, bias="none")
+    t = inputs.make_inputs(p, 1, "cuda")
+    cfg = moe.MoeConfig(d=d, E=1, k=1, I=128, n_shared=1, I_shared=Is, dtype="bf16", weight_layout="packed")
+    sg, sd = moe.pack_shared_weights(cfg, t["ws_gate"], t["ws_up"], t["ws_down"])
+    ws = moe.alloc_workspace(cfg, T)
+    out = torch.full((T, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    moe.moe_shared_ffn(cfg, T, t["x"], sg, None, sd, out, ws)
+    torch.cuda.synchronize()
+    want = O.swiglu_ffn(inputs.oracle_view(t["x"]), inputs.oracle_view(t["ws_gate"]),
+                        inputs.oracle_view(t["ws_up"]), inputs.oracle_view(t["ws_down"]))
+    got = host(out.float())
+    assert np.isfinite(got).all(), "rows left unwritten"
+    assert max_rel_err(got, want) <= BF16_TOL
+
+
 # ---------------------------------------------------------------------------
 # moe_combine
 # ---------------------------------------------------------------------------

@@ -80,9 +80,12 @@ def test_layer_deterministic_across_runs_and_streams():
     assert torch.equal(a["out"], d["out"])
 
 
-@pytest.mark.parametrize("name", ["dsv3_like_bf16", "decode_like_bf16"])
-def test_layer_packed_matches_rowmajor(name):
-    p = dict(SMALL[name], d=512, I=256)   # packed weights need I % 128 == 0 and d % 256 == 0
+@pytest.mark.parametrize("name,I_shared", [("dsv3_like_bf16", 256),    # shared expert fused into the routed GEMMs
+                                           ("dsv3_like_bf16", 128),    # shared expert on its own (I_shared != I)
+                                           ("decode_like_bf16", 256)])
+def test_layer_packed_matches_rowmajor(name, I_shared):
+    # packed weights need I, I_shared % 128 == 0 and d % 256 == 0
+    p = dict(SMALL[name], d=512, I=256, I_shared=I_shared)
     t = G.device_inputs(p, seed=5)
     ref = G.run_layer(p, t)
     routing = G.check_routing_and_dispatch_exact(p, t, ref)
@@ -91,7 +94,11 @@ def test_layer_packed_matches_rowmajor(name):
     for key in ("logits", "topk_idx", "topk_w", "counts", "offsets", "sorted_token", "inv_perm"):
         assert torch.equal(ref[key], r[key]), key
     assert max_rel_err(G.host(r["y_perm"].float()), y) <= G.tol(p)
+    assert max_rel_err(G.host(r["shared_out"].float()), sh) <= G.tol(p)
     assert max_rel_err(G.host(r["out"].float()), out) <= G.tol(p)
+    for s_aux in (None, "new"):   # same bits on one stream or two
+        r2 = G.run_layer(dict(p, weight_layout="packed"), t, s_aux=s_aux)
+        assert torch.equal(r2["out"], r["out"])
 
 
 def test_layer_on_side_streams():
