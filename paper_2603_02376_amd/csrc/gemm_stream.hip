@@ -14,9 +14,11 @@
 //   * Weights for kDepth-1 steps ahead stay in flight per wave (a ring of
 //     register sets, the K loop unrolled so every set is statically indexed).
 //   * The token rows (A, gathered through sorted_token) are shared by the 4
-//     waves through a two-slot LDS ring: each wave loads its share of the
-//     next step's rows into registers and writes them to the free slot at
-//     the end of the step; one barrier per step publishes them. Only
+//     waves through a three-slot LDS ring: each wave loads its share of a
+//     step's rows into registers three steps ahead and writes them to the
+//     ring two steps ahead; one barrier per step publishes them. The first
+//     K slice of the next step is read before that barrier, so neither the
+//     row loads nor LDS latency sit on the per-step critical path. Only
 //     register loads are in flight, so the compiler's load-count waits are
 //     exact. (Direct-to-LDS loads mixed with register loads under partial
 //     vmcnt waits were observed to read stale LDS data: their completions
@@ -33,8 +35,9 @@
 //     through L2.
 //   * The K loop is compiled per count of active 32-row fragments, so the
 //     MFMA stream has no branches.
-//   * The epilogue stages each 32-row fragment through a wave-private LDS
-//     tile and stores whole 16-byte runs of output rows.
+//   * The MFMAs take the weights as their first operand and the token rows
+//     as their second, so every lane ends with runs of 4 consecutive output
+//     columns of one token row and stores them directly (no LDS transpose).
 //
 // Packed layout (element = bf16, 8 per 16-byte lane chunk), per expert:
 //   GEMM1: [I/128 tiles][K/64 steps][4 waves][4 kk][2 j][64 lanes][8]
@@ -56,11 +59,15 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxRows = 192;      // rows per pass
 constexpr int kStepBytes = 8192;   // one wave's weights per K step
-constexpr int kDepth = 4;          // weight register sets: the current K step and kDepth-1 in flight
-constexpr int kSlots = 2;          // A ring slots in LDS: the current step and the next
-constexpr int kUnroll = (kDepth % kSlots == 0) ? kDepth : kDepth * kSlots;  // K-loop unroll
+constexpr int kDepth = 3;          // weight register sets: the current K step and kDepth-1 in flight
+constexpr int kSlots = 3;          // A ring slots in LDS: the current step, the next, the one being written
+constexpr int kStage = 2;          // A register sets: rows loaded three steps ahead, written two ahead
+constexpr int kUnroll = 6;         // K-loop unroll: a multiple of kDepth, kSlots and kStage
+static_assert(kUnroll % kDepth == 0 && kUnroll % kSlots == 0 && kUnroll % kStage == 0, "unroll");
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
 // A ring layout: 128-byte rows of 8 16-byte chunks, chunk c of row r stored at
 // chunk c ^ ((r >> 1) & 7). The 16 rows one quarter-wave reads with a 16-byte
@@ -115,8 +122,7 @@ template <int EPI>
 __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
   constexpr int WCOLS = (EPI == EPI_SWIGLU) ? 32 : 64;  // output columns per wave
   constexpr int TCOLS = WCOLS * kWaves;                  // per tile
-  // Dynamic LDS: the A ring (kSlots slots of kMaxRows x 128 bytes), then one
-  // 32-row output staging tile per wave.
+  // Dynamic LDS: the A ring (kSlots slots of kMaxRows x 128 bytes).
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int tstart[257];
   __shared__ int scan_scratch[kWaves];
@@ -238,64 +244,62 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         const int ar = gather ? min(max(gather[row0 + r], 0), a_rows - 1) : row0 + r;
         a_off[i] = (uint32_t)ar * (uint32_t)(K * 2) + lc * 16;
       }
-      // Registers per in-flight K step: this wave's weights (kDepth sets: a
-      // step's weights are loaded kDepth-1 steps ahead) and its share of the next
-      // step's A rows (one set: loaded one step ahead, written to the LDS
-      // ring at the end of the step). Every load returns to registers, so the
-      // compiler's own wait counts (in-order returns) are exact and no
-      // hand-written vmcnt wait is needed.
+      // Per wave, in flight: weights for kDepth-1 steps ahead (kDepth register
+      // sets) and its share of the A rows of the steps two and three ahead
+      // (kStage register sets, written to the LDS ring two steps before use).
+      // Every load returns to registers, so the compiler's own wait counts
+      // (in-order returns) are exact and no hand-written vmcnt wait is needed.
       i32x4 bq[kDepth][8];
-      i32x4 sa[A_CH];
+      i32x4 sa[kStage][A_CH];
       // Steps past the end are clamped to the last one: those surplus loads
       // are never used, which keeps the steady-state loop free of branches.
-      auto load_a = [&](int ks, int i) {
+      auto load_a = [&](int ks, auto s_c, int i) {
         const int kc = min(ks, nk - 1);
-        sa[i] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, (int)(a_off[i] + kc * 128), 0, 0);
+        sa[decltype(s_c)::value][i] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, (int)(a_off[i] + kc * 128), 0, 0);
       };
       auto load_b = [&](int ks, auto s_c, int n) {
-        constexpr int S = decltype(s_c)::value;
         const int kc = min(ks, nk - 1);
-        bq[S][n] = __builtin_nontemporal_load(
+        bq[decltype(s_c)::value][n] = __builtin_nontemporal_load(
             reinterpret_cast<const i32x4*>(bw + (size_t)kc * kWaves * kStepBytes + n * 1024));
       };
-      // Write the staged A rows into ring slot S (layout of lds_off(): lane l
+      // Write A register set S into ring slot R (layout of lds_off(): lane l
       // holds row l/8 of each 8-row block, at physical chunk l%8).
-      auto stage = [&](auto s_c) {
-        constexpr int S = decltype(s_c)::value;
-        char* const dst = smem + S * (kMaxRows * 128) + wave * 8 * 128 + lane * 16;
+      auto stage = [&](auto s_c, auto r_c) {
+        char* const dst = smem + decltype(r_c)::value * (kMaxRows * 128) + wave * 8 * 128 + lane * 16;
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<i32x4*>(dst + i * 8 * kWaves * 128) = sa[i];
+        for (int i = 0; i < A_CH; ++i)
+          *reinterpret_cast<i32x4*>(dst + i * 8 * kWaves * 128) = sa[decltype(s_c)::value][i];
       };
 
       auto kloop = [&](auto nact_c) {
         constexpr int NACT = decltype(nact_c)::value;
-        // Step ks (U = ks % kUnroll) multiplies with weight set U % kDepth and
-        // ring slot U % kSlots, loads step ks+1's A rows and step
-        // ks+kDepth-1's weights and, at its end, writes the A rows into the
-        // other ring slot, whose previous reader (step ks-1) left it before the
-        // barrier of step ks.
+        auto rd = [&](int slot, int kk, int i) {
+          return *reinterpret_cast<const i32x4*>(smem + slot * (kMaxRows * 128) +
+                                                 lds_off(32 * i + (lane & 31), 2 * kk + (lane >> 5)));
+        };
+        i32x4 af[NACT > 0 ? NACT : 1];  // A fragments of the current 16-wide K slice
+        // Step ks (U = ks % kUnroll) multiplies slot U % kSlots with weight set
+        // U % kDepth while loading step ks+3's A rows and step ks+kDepth-1's
+        // weights. At its end it writes step ks+2's A rows into slot
+        // (U+2) % kSlots (last read by step ks-1, which every wave finished
+        // before the previous barrier), reads the first K slice of step ks+1
+        // (published by the previous barrier) and meets the others at a
+        // barrier, so no LDS latency sits between the barrier and the MFMAs.
         auto step = [&](int ks, auto u_c) {
           constexpr int U = decltype(u_c)::value;
-          constexpr int BS = U % kDepth;
-          constexpr auto S1 = std::integral_constant<int, (U + 1) % kSlots>{};
+          constexpr int SL = U % kSlots, BS = U % kDepth;
           constexpr auto SB = std::integral_constant<int, (U + kDepth - 1) % kDepth>{};
-          lds_barrier();  // slot U written by every wave
+          constexpr auto SA3 = std::integral_constant<int, (U + 3) % kStage>{};  // set of step ks+3
+          constexpr auto SA2 = std::integral_constant<int, (U + 2) % kStage>{};  // set of step ks+2
+          constexpr auto SL2 = std::integral_constant<int, (U + 2) % kSlots>{};
           __builtin_amdgcn_sched_barrier(0);
           if constexpr (NACT > 0) {
             // Fixed instruction order (each group closed by a scheduling
-            // barrier): the first 16-wide K slice of A, then per row fragment
-            // the two MFMAs of one slice, the read of the same fragment's next
-            // slice (NACT groups to land) and an even share of this step's
-            // loads (A rows first). Spreading the loads keeps a load that
-            // waits for queue space from idling the matrix core for long.
-            const char* as = smem + (U % kSlots) * (kMaxRows * 128);
-            auto rd = [&](int kk, int i) {
-              return *reinterpret_cast<const i32x4*>(as + lds_off(32 * i + (lane & 31), 2 * kk + (lane >> 5)));
-            };
-            i32x4 af[NACT];
-#pragma unroll
-            for (int i = 0; i < NACT; ++i) af[i] = rd(0, i);
-            __builtin_amdgcn_sched_barrier(0);
+            // barrier): per row fragment the two MFMAs of one slice, the read
+            // of the same fragment's next slice (NACT groups to land) and an
+            // even share of this step's loads (A rows first). Spreading the
+            // loads keeps a load that waits for queue space from idling the
+            // matrix core for long.
             constexpr int GROUPS = 4 * NACT;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
@@ -304,13 +308,13 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
                 const int g = kk * NACT + i;
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[i]),
-                                                                      __builtin_bit_cast(bf16x8, bq[BS][kk * 2 + j]),
+                  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bq[BS][kk * 2 + j]),
+                                                                      __builtin_bit_cast(bf16x8, af[i]),
                                                                       acc[i][j], 0, 0, 0);
-                if (kk < 3) af[i] = rd(kk + 1, i);
+                if (kk < 3) af[i] = rd(SL, kk + 1, i);
 #pragma unroll
                 for (int n = g * LOADS / GROUPS; n < (g + 1) * LOADS / GROUPS; ++n) {
-                  if (n < A_CH) load_a(ks + 1, n);
+                  if (n < A_CH) load_a(ks + 3, SA3, n);
                   else load_b(ks + kDepth - 1, SB, n - A_CH);
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -318,20 +322,33 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
             }
           } else {
 #pragma unroll
-            for (int i = 0; i < A_CH; ++i) load_a(ks + 1, i);
+            for (int i = 0; i < A_CH; ++i) load_a(ks + 3, SA3, i);
 #pragma unroll
             for (int n = 0; n < 8; ++n) load_b(ks + kDepth - 1, SB, n);
           }
-          stage(S1);
+          stage(SA2, SL2);
+          lds_wait();  // this wave's ring writes (and reads) are done
+#pragma unroll
+          for (int i = 0; i < NACT; ++i) af[i] = rd((U + 1) % kSlots, 0, i);
+          barrier_only();
         };
         lds_barrier();  // every wave is done with the previous tile's ring
+        static_for<kStage>([&](auto s_c) {
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) load_a(0, i);
+          for (int i = 0; i < A_CH; ++i) load_a(decltype(s_c)::value, s_c, i);
+        });
         static_for<kDepth - 1>([&](auto s_c) {
 #pragma unroll
           for (int n = 0; n < 8; ++n) load_b(decltype(s_c)::value, s_c, n);
         });
-        stage(std::integral_constant<int, 0>{});
+        stage(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+        stage(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{});
+        // step 2's rows take set 0 (free again); step 0 then loads step 3's
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i) load_a(2, std::integral_constant<int, 0>{}, i);
+        lds_barrier();  // slots 0 and 1 written by every wave
+#pragma unroll
+        for (int i = 0; i < NACT; ++i) af[i] = rd(0, 0, i);
         int ks = 0;
         for (; ks + kUnroll <= nk; ks += kUnroll) static_for<kUnroll>([&](auto u_c) { step(ks + u_c, u_c); });
         static_for<kUnroll - 1>([&](auto u_c) {
@@ -343,33 +360,35 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     if (rows <= 128) body(std::integral_constant<int, 128>{});
     else body(std::integral_constant<int, kMaxRows>{});
 
-    // ---- epilogue: one 32-row fragment at a time through a wave-private LDS
-    // tile, so each lane stores whole 16-byte runs of an output row.
-    char* const stg = smem + kSlots * kMaxRows * 128 + wave * (32 * WCOLS * 2);
+    // ---- epilogue. The MFMAs take the weights as their first operand, so
+    // acc[i][j] is the transposed 32x32 tile: lane l holds token row
+    // 32 i + l%32 and output columns 32 j + 8 g + 4 (l/32) + 0..3 in
+    // registers 4 g .. 4 g + 3, which it stores as one 8-byte run per g.
     __bf16* const C = c_base;
     const size_t ldc = (size_t)p.ldc;
-    const int colbase = nt * TCOLS + wave * WCOLS;
-    constexpr int RCH = WCOLS / 8;  // 16-byte chunks per staged row
+    const int colbase = nt * TCOLS + wave * WCOLS + 4 * (lane >> 5);
 #pragma unroll
     for (int i = 0; i < kMaxRows / 32; ++i) {
       if (i >= nact) break;
+      const int orow = 32 * i + (lane & 31);
+      if (orow >= rows) continue;
+      __bf16* const crow = C + (size_t)(row0 + orow) * ldc + colbase;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        __bf16* const srow = reinterpret_cast<__bf16*>(stg) + row * WCOLS + (lane & 31);
+      for (int g = 0; g < 4; ++g) {
         if (EPI == EPI_SWIGLU) {
-          srow[0] = static_cast<__bf16>(silu_f(acc[i][0][r]) * acc[i][1][r]);
-        } else {
-          srow[0] = static_cast<__bf16>(acc[i][0][r]);
-          srow[32] = static_cast<__bf16>(acc[i][1][r]);
-        }
-      }
+          bf16x4 v;
 #pragma unroll
-      for (int t = 0; t < 32 * RCH / 64; ++t) {
-        const int q = lane + 64 * t, row = q / RCH, cc = q % RCH;
-        const i32x4 v = *reinterpret_cast<const i32x4*>(stg + row * (WCOLS * 2) + cc * 16);
-        const int orow = 32 * i + row;
-        if (orow < rows) *reinterpret_cast<i32x4*>(C + (size_t)(row0 + orow) * ldc + colbase + cc * 8) = v;
+          for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(silu_f(acc[i][0][4 * g + e]) * acc[i][1][4 * g + e]);
+          *reinterpret_cast<bf16x4*>(crow + 8 * g) = v;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            bf16x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(acc[i][j][4 * g + e]);
+            *reinterpret_cast<bf16x4*>(crow + 32 * j + 8 * g) = v;
+          }
+        }
       }
     }
   }
@@ -409,7 +428,7 @@ __global__ void pack_kernel(const __bf16* __restrict__ w0, const __bf16* __restr
 template <int EPI>
 hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
   auto kern = gemm_stream_kernel<EPI>;
-  constexpr size_t lds = (size_t)kSlots * kMaxRows * 128 + kWaves * 32 * ((EPI == EPI_SWIGLU) ? 32 : 64) * 2;
+  constexpr size_t lds = (size_t)kSlots * kMaxRows * 128;
   static std::once_flag once;
   static hipError_t init_err = hipSuccess;
   std::call_once(once, [&] {
