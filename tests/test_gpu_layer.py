@@ -115,7 +115,8 @@ def test_layer_on_side_streams():
 # full workload sizes (sampled outputs)
 # ---------------------------------------------------------------------------
 
-FULL = ["dsv3", "dsv3_packed", "dsv3_skew", "dsv3_decode", "mixtral"]
+# every full-size workload in both weight layouts (bench.py times the packed one)
+FULL = [w + lay for w in ("dsv3", "dsv3_skew", "dsv3_decode", "mixtral") for lay in ("", "_packed")]
 SAMPLE = 8
 
 
@@ -150,5 +151,5 @@ def test_layer_full_size_sampled(name):
         want_sh = O.swiglu_ffn(inputs.oracle_view(t["x"])[rows], *(inputs.oracle_view(s) for s in sh))
         assert max_rel_err(G.host(r["shared_out"].float())[rows], want_sh) <= G.tol(p)
     del r
-    if name == "mixtral":
+    if name.startswith("mixtral") and name.endswith("_packed"):
         G.release_cached_weights()
