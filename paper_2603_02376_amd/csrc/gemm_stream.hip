@@ -37,7 +37,10 @@
 //     MFMA stream has no branches.
 //   * The MFMAs take the weights as their first operand and the token rows
 //     as their second, so every lane ends with runs of 4 consecutive output
-//     columns of one token row and stores them directly (no LDS transpose).
+//     columns of one token row. The epilogue assembles the output tile in
+//     LDS and writes it in whole 128-byte lines with streaming stores that
+//     bypass L2, so the outputs do not evict the token rows that the column
+//     tiles of one expert share through L2.
 //
 // Packed layout (element = bf16, 8 per 16-byte lane chunk), per expert:
 //   GEMM1: [I/128 tiles][K/64 steps][4 waves][4 kk][2 j][64 lanes][8]
@@ -48,6 +51,7 @@
 //   The 8 elements of (step s, kk, lane) are k = s*64 + kk*16 + 8*(lane>>5) + 0..7.
 #include "moe_internal.h"
 
+#include <algorithm>
 #include <mutex>
 #include <type_traits>
 #include <utility>
@@ -63,6 +67,7 @@ constexpr int kDepth = 3;          // weight register sets: the current K step a
 constexpr int kSlots = 3;          // A ring slots in LDS: the current step, the next, the one being written
 constexpr int kStage = 2;          // A register sets: rows loaded three steps ahead, written two ahead
 constexpr int kUnroll = 6;         // K-loop unroll: a multiple of kDepth, kSlots and kStage
+constexpr int kStreamStore = 19;   // cache policy of output stores: sc0 sc1 nt (streaming, not kept in L2)
 static_assert(kUnroll % kDepth == 0 && kUnroll % kSlots == 0 && kUnroll % kStage == 0, "unroll");
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -363,31 +368,60 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     // ---- epilogue. The MFMAs take the weights as their first operand, so
     // acc[i][j] is the transposed 32x32 tile: lane l holds token row
     // 32 i + l%32 and output columns 32 j + 8 g + 4 (l/32) + 0..3 in
-    // registers 4 g .. 4 g + 3, which it stores as one 8-byte run per g.
-    __bf16* const C = c_base;
-    const size_t ldc = (size_t)p.ldc;
-    const int colbase = nt * TCOLS + wave * WCOLS + 4 * (lane >> 5);
+    // registers 4 g .. 4 g + 3. Those 8-byte runs go into an LDS copy of the
+    // output tile (rows x TCOLS bf16, 16-byte chunks XOR-swizzled by row);
+    // the tile then leaves in whole 128-byte lines, one 16-byte chunk per
+    // thread per pass, OROWS rows per pass, as streaming stores that bypass
+    // L2 (written once, read by a later kernel): write-allocated output
+    // lines would evict the token rows the column tiles share through L2.
+    {
+      constexpr int OCH = TCOLS * 2 / 16;      // 16-byte chunks per output row
+      constexpr int OROWS = kThreads / OCH;    // rows per store pass
+      lds_barrier();                           // every wave is done reading the A ring
+      const int h = lane >> 5;
 #pragma unroll
-    for (int i = 0; i < kMaxRows / 32; ++i) {
-      if (i >= nact) break;
-      const int orow = 32 * i + (lane & 31);
-      if (orow >= rows) continue;
-      __bf16* const crow = C + (size_t)(row0 + orow) * ldc + colbase;
+      for (int i = 0; i < kMaxRows / 32; ++i) {
+        __builtin_amdgcn_sched_barrier(0);  // one fragment at a time: few live registers
+        if (i < nact) {
+          const int r = 32 * i + (lane & 31);
+          char* const orow = smem + r * (TCOLS * 2);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        if (EPI == EPI_SWIGLU) {
-          bf16x4 v;
+          for (int g = 0; g < 4; ++g) {
+            if (EPI == EPI_SWIGLU) {
+              bf16x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(silu_f(acc[i][0][4 * g + e]) * acc[i][1][4 * g + e]);
-          *reinterpret_cast<bf16x4*>(crow + 8 * g) = v;
-        } else {
+              for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(silu_f(acc[i][0][4 * g + e]) * acc[i][1][4 * g + e]);
+              const int c = wave * 4 + g;
+              *reinterpret_cast<bf16x4*>(orow + ((c ^ (r & 7)) << 4) + 8 * h) = v;
+            } else {
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            bf16x4 v;
+              for (int j = 0; j < 2; ++j) {
+                bf16x4 v;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(acc[i][j][4 * g + e]);
-            *reinterpret_cast<bf16x4*>(crow + 32 * j + 8 * g) = v;
+                for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(acc[i][j][4 * g + e]);
+                const int c = wave * 8 + 4 * j + g;
+                *reinterpret_cast<bf16x4*>(orow + ((c ^ (r & 7)) << 4) + 8 * h) = v;
+              }
+            }
           }
+        }
+      }
+      lds_barrier();
+      const size_t ldc = (size_t)p.ldc;
+      char* const cb = reinterpret_cast<char*>(c_base) + ((size_t)row0 * ldc + (size_t)nt * TCOLS) * 2;
+      // rows >= `rows` fall outside the buffer range: the hardware drops them
+      const __amdgpu_buffer_rsrc_t c_rs =
+          __builtin_amdgcn_make_buffer_rsrc(cb, (short)0, (int)((uint32_t)rows * (uint32_t)(ldc * 2)), 0x00020000);
+      const int oc = tid % OCH;
+      const int npass = (rows + OROWS - 1) / OROWS;
+#pragma unroll
+      for (int q = 0; q < kMaxRows / OROWS; ++q) {
+        if (q % 4 == 0) __builtin_amdgcn_sched_barrier(0);  // a few rows in flight: few live registers
+        if (q < npass) {
+          const int r = q * OROWS + tid / OCH;
+          const i32x4 v = *reinterpret_cast<const i32x4*>(smem + r * (TCOLS * 2) + ((oc ^ (r & 7)) << 4));
+          __builtin_amdgcn_raw_buffer_store_b128(v, c_rs, (int)((uint32_t)r * (uint32_t)(ldc * 2) + oc * 16), 0,
+                                                 kStreamStore);
         }
       }
     }
@@ -428,7 +462,9 @@ __global__ void pack_kernel(const __bf16* __restrict__ w0, const __bf16* __restr
 template <int EPI>
 hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
   auto kern = gemm_stream_kernel<EPI>;
-  constexpr size_t lds = (size_t)kSlots * kMaxRows * 128;
+  // the A ring, reused after each tile's K loop as the LDS copy of its output
+  constexpr size_t lds = std::max<size_t>((size_t)kSlots * kMaxRows * 128,
+                                          (size_t)kMaxRows * ((EPI == EPI_SWIGLU) ? 128 : 256) * 2);
   static std::once_flag once;
   static hipError_t init_err = hipSuccess;
   std::call_once(once, [&] {
