@@ -290,8 +290,13 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         // before the previous barrier), reads the first K slice of step ks+1
         // (published by the previous barrier) and meets the others at a
         // barrier, so no LDS latency sits between the barrier and the MFMAs.
-        auto step = [&](int ks, auto u_c) {
+        // TAIL: one of the last steps, whose loads past the last K step are
+        // skipped (elsewhere every load is in range, and the loads stay
+        // unconditional so the compiler's wait counts are exact).
+        auto step = [&](int ks, auto u_c, auto tail_c) {
           constexpr int U = decltype(u_c)::value;
+          constexpr bool TAIL = decltype(tail_c)::value;
+          const bool a_ok = !TAIL || ks + 3 < nk, b_ok = !TAIL || ks + kDepth - 1 < nk;
           constexpr int SL = U % kSlots, BS = U % kDepth;
           constexpr auto SB = std::integral_constant<int, (U + kDepth - 1) % kDepth>{};
           constexpr auto SA3 = std::integral_constant<int, (U + 3) % kStage>{};  // set of step ks+3
@@ -319,17 +324,22 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
                 if (kk < 3) af[i] = rd(SL, kk + 1, i);
 #pragma unroll
                 for (int n = g * LOADS / GROUPS; n < (g + 1) * LOADS / GROUPS; ++n) {
-                  if (n < A_CH) load_a(ks + 3, SA3, n);
-                  else load_b(ks + kDepth - 1, SB, n - A_CH);
+                  if (n < A_CH) {
+                    if (a_ok) load_a(ks + 3, SA3, n);
+                  } else if (b_ok) {
+                    load_b(ks + kDepth - 1, SB, n - A_CH);
+                  }
                 }
                 __builtin_amdgcn_sched_barrier(0);
               }
             }
           } else {
 #pragma unroll
-            for (int i = 0; i < A_CH; ++i) load_a(ks + 3, SA3, i);
+            for (int i = 0; i < A_CH; ++i)
+              if (a_ok) load_a(ks + 3, SA3, i);
 #pragma unroll
-            for (int n = 0; n < 8; ++n) load_b(ks + kDepth - 1, SB, n);
+            for (int n = 0; n < 8; ++n)
+              if (b_ok) load_b(ks + kDepth - 1, SB, n);
           }
           stage(SA2, SL2);
           lds_wait();  // this wave's ring writes (and reads) are done
@@ -355,9 +365,11 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
 #pragma unroll
         for (int i = 0; i < NACT; ++i) af[i] = rd(0, 0, i);
         int ks = 0;
-        for (; ks + kUnroll <= nk; ks += kUnroll) static_for<kUnroll>([&](auto u_c) { step(ks + u_c, u_c); });
-        static_for<kUnroll - 1>([&](auto u_c) {
-          if (ks + u_c < nk) step(ks + u_c, u_c);
+        // main loop: every load of its steps is in range (ks + kUnroll + 2 < nk)
+        for (; ks + kUnroll + 2 < nk; ks += kUnroll)
+          static_for<kUnroll>([&](auto u_c) { step(ks + u_c, u_c, std::false_type{}); });
+        static_for<kUnroll + 2>([&](auto u_c) {
+          if (ks + u_c < nk) step(ks + u_c, std::integral_constant<int, decltype(u_c)::value % kUnroll>{}, std::true_type{});
         });
       };
       with_count<AR / 32>(min(nact, AR / 32), kloop);
