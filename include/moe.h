@@ -44,7 +44,9 @@
  *    MOE_LAYOUT_PACKED (see moe_pack_weights).
  *    Inputs must be finite.
  *  - Results are deterministic: two calls on the same inputs give the same
- *    bits, whatever the stream arrangement (no atomics decide any order).
+ *    bits, whatever the stream arrangement. (With packed weights the expert
+ *    GEMMs hand out tiles to workgroups through atomic counters, but every
+ *    output element is still computed in one fixed order.)
  *  - Calls that share one workspace must not overlap in time.
  */
 #ifndef MOE_H
@@ -165,7 +167,8 @@ int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, in
  *   h[r]      = silu(x[sorted_token[r]] · w_gate[e]ᵀ) * (x[sorted_token[r]] · w_up[e]ᵀ)
  *   y_perm[r] = h[r] · w_down[e]ᵀ
  * The row gather is fused into the GEMM's operand load. h lives in the
- * workspace (dtype, [T*k][I]).
+ * workspace (dtype, [T*k][I]); with packed weights so do the GEMMs' tile-queue
+ * heads, which the call resets before its first GEMM.
  *  y_perm : [T*k][d] dtype out.
  */
 int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x,

@@ -44,10 +44,15 @@ int gate_splits(const moe_config_t& c, int32_t T) {
   return (nkt + q - 1) / q;  // no empty split
 }
 
+// Tile-queue heads of the weight-streaming GEMMs: 8 per launch, GEMM1 and
+// GEMM2 of the routed FFN, then of the shared expert's own FFN (which may run
+// on another stream at the same time).
+constexpr int kQueueInts = 32;
+
 // Byte offsets of every scratch region inside the caller's workspace.
 struct Layout {
   size_t gate_partials, logits, topk_idx, topk_w, masks, bases, counts, offsets, sorted_token, sorted_assign,
-      inv_perm, h, y_perm, shared_h, shared_out, total;
+      inv_perm, h, y_perm, shared_h, shared_out, queues, total;
 };
 
 Layout make_layout(const moe_config_t& c, int32_t T) {
@@ -76,6 +81,7 @@ Layout make_layout(const moe_config_t& c, int32_t T) {
   L.y_perm = take(tk * c.d * es);
   L.shared_h = take(c.n_shared ? t * c.I_shared * es : 0);
   L.shared_out = take(c.n_shared ? t * c.d * es : 0);
+  L.queues = take(kQueueInts * 4);
   L.total = off;
   return L;
 }
@@ -224,9 +230,15 @@ struct FusedShared {
 // y = h Wdᵀ into `y`. packed: weights from moe_pack_weights (wu unused) and
 // the weight-streaming kernel; fused (packed only, same intermediate size):
 // the shared expert over all a_rows tokens rides along as an extra group.
+// queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path.
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
-                   void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr) {
+                   void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
+                   int32_t* queues = nullptr) {
+  if (packed && queues) {
+    const hipError_t e = moe::launch_queue_reset(queues, 16, s);
+    if (e != hipSuccess) return e;
+  }
   moe::GemmProblem up{};
   up.A = x;
   up.a_rows = a_rows;
@@ -246,6 +258,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
     up.xC = fused->h;
     up.x_rows = a_rows;
   }
+  up.tile_queue = queues;
   hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
   if (e != hipSuccess) return e;
   moe::GemmProblem down{};
@@ -265,6 +278,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
     down.xC = fused->out;
     down.x_rows = a_rows;
   }
+  down.tile_queue = queues ? queues + 8 : nullptr;
   return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
@@ -385,7 +399,8 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   if (T == 0) return MOE_OK;
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
-                               static_cast<char*>(ws) + L.h, y_perm, stream, packed);
+                               static_cast<char*>(ws) + L.h, y_perm, stream, packed, nullptr,
+                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues));
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
 }
 
@@ -403,7 +418,8 @@ int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void
   if (T == 0) return MOE_OK;
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T, 1, cfg->I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down,
-                               static_cast<char*>(ws) + L.shared_h, out, stream, packed);
+                               static_cast<char*>(ws) + L.shared_h, out, stream, packed, nullptr,
+                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues) + 16);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "shared FFN");
 }
 
@@ -460,6 +476,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   int32_t* inv = d.inv_perm ? d.inv_perm : reinterpret_cast<int32_t*>(w + L.inv_perm);
   void* y = d.y_perm ? d.y_perm : w + L.y_perm;
   void* shared = c.n_shared ? (d.shared_out ? d.shared_out : w + L.shared_out) : nullptr;
+  int32_t* const queues = reinterpret_cast<int32_t*>(w + L.queues);  // routed FFN: [0, 16), shared FFN: [16, 32)
 
   hipError_t e;
   // Packed weights with equal intermediate sizes: the shared expert runs
@@ -475,7 +492,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     if ((e = hipEventRecord(ev->fork, s_main)) != hipSuccess) return hip_fail(e, "event record");
     if ((e = hipStreamWaitEvent(s_aux, ev->fork, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h, shared,
-                     s_aux, packed)) != hipSuccess)
+                     s_aux, packed, nullptr, queues + 16)) != hipSuccess)
       return hip_fail(e, "shared FFN");
     if ((e = hipEventRecord(ev->join, s_aux)) != hipSuccess) return hip_fail(e, "event record");
   }
@@ -492,13 +509,13 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     fs.out = shared;
   }
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main, packed,
-                   fuse ? &fs : nullptr)) != hipSuccess)
+                   fuse ? &fs : nullptr, queues)) != hipSuccess)
     return hip_fail(e, "expert FFN");
   if (c.n_shared && !fuse) {
     if (two) {
       if ((e = hipStreamWaitEvent(s_main, ev->join, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     } else if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h,
-                            shared, s_main, packed)) != hipSuccess) {
+                            shared, s_main, packed, nullptr, queues + 16)) != hipSuccess) {
       return hip_fail(e, "shared FFN");
     }
   }

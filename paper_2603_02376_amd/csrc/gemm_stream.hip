@@ -163,14 +163,28 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   auto seg_start = [&](int j) { return (int)((int64_t)j * routed_tiles / Nt) + j * units_x; };
   const int nk = p.K / 64;
   const int G = gridDim.x, b = blockIdx.x;
-  const int vb = (G % 8 == 0) ? (b % 8) * (G / 8) + (b / 8) : b;
+  // Schedule. Workgroups are dealt to the 8 XCDs round-robin (b % 8); XCD x
+  // owns the queue of tiles {r G + x W + j : j < W} (W = G / 8, r = 0, 1,
+  // ...), so adjacent tiles (an expert's column tiles, sharing token rows
+  // through L2) run on one XCD. Each workgroup starts with queue entry b / 8
+  // and then claims entries W, W + 1, ... from its XCD's queue head; when its
+  // queue is empty it takes tiles from the other XCDs' queues. Without queue
+  // heads it takes every G-th tile.
+  const bool dyn = p.tile_queue != nullptr && G % 8 == 0;
+  const int W = G / 8, xcd = b % 8;
+  auto qtile = [&](int x, int q) { return (q / W) * G + x * W + q % W; };
+  const int vb = (G % 8 == 0) ? xcd * W + (b / 8) : b;
+  __shared__ int s_next;
   const int K = p.K;
   // A rows move in 1 KB blocks of 8 rows (block b of a wave: rows 32b + 8 wave
   // + 0..7): lane l carries row l/8 of the block and the logical 16-byte chunk
   // that lds_off() places at physical chunk l%8.
   const int lr = lane >> 3, lc = (lane & 7) ^ ((wave * 4 + (lr >> 1)) & 7);
 
-  for (int tile = vb; tile < total_tiles; tile += G) {
+  for (int tile = vb; tile < total_tiles;) {
+    // claim the next entry of this XCD's queue now; it is used after this tile
+    int claim = 0;
+    if (dyn && tid == 0) claim = atomicAdd(&p.tile_queue[xcd], 1);
     // ---- decode: group, pass and column tile nt
     int seg = 0;
     if (units_x > 0) {
@@ -389,6 +403,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     {
       constexpr int OCH = TCOLS * 2 / 16;      // 16-byte chunks per output row
       constexpr int OROWS = kThreads / OCH;    // rows per store pass
+      if (tid == 0) s_next = dyn ? qtile(xcd, W + claim) : tile + G;
       lds_barrier();                           // every wave is done reading the A ring
       const int h = lane >> 5;
 #pragma unroll
@@ -437,7 +452,26 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         }
       }
     }
+    tile = s_next;  // written before the epilogue's barriers
+    if (dyn && tile >= total_tiles) {
+      // this XCD's queue is empty: take a tile from another XCD's queue
+      __syncthreads();  // every thread has read s_next
+      if (tid == 0) {
+        int t = total_tiles;
+        for (int k = 1; k < 8 && t >= total_tiles; ++k) {
+          const int x = (xcd + k) % 8;
+          t = qtile(x, W + atomicAdd(&p.tile_queue[x], 1));
+        }
+        s_next = t;
+      }
+      __syncthreads();
+      tile = s_next;
+    }
   }
+}
+
+__global__ void queue_reset_kernel(int32_t* q, int n) {
+  if ((int)threadIdx.x < n) q[threadIdx.x] = 0;
 }
 
 // One 16-byte chunk per thread: packed position -> source row and k.
@@ -506,6 +540,12 @@ hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
   if ((p.M <= 0 && p.x_rows <= 0) || p.N <= 0) return hipSuccess;
   if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU>(p, s);
   return launch_stream<EPI_STORE>(p, s);
+}
+
+hipError_t launch_queue_reset(int32_t* q, int n, hipStream_t s) {
+  if (!q || n <= 0 || n > 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(queue_reset_kernel, dim3(1), dim3(64), 0, s, q, n);
+  return hipGetLastError();
 }
 
 hipError_t launch_pack(const void* w0, const void* w1, void* dst, int E, int N, int K, bool gate_up, hipStream_t s) {

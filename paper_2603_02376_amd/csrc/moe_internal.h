@@ -59,6 +59,10 @@ struct GemmProblem {
   const void* xB;
   void* xC;
   int32_t x_rows;
+  // Weight-streaming kernel only: 8 queue heads (one per XCD), zero at
+  // launch, from which workgroups claim tiles after their first (nullptr:
+  // a static round-robin schedule).
+  int32_t* tile_queue;
 };
 
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
@@ -67,6 +71,9 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, int epilogue, bool out_f32, hi
 // Weight-streaming bf16 grouped GEMM over packed weights (B0 = packed buffer;
 // N % 128 == 0 for EPI_SWIGLU, N % 256 == 0 for EPI_STORE, K % 64 == 0).
 hipError_t launch_gemm_stream(const GemmProblem& p, int epilogue, hipStream_t s);
+// Zeroes n queue heads of launch_gemm_stream (a one-workgroup kernel, so
+// it can be captured in a graph).
+hipError_t launch_queue_reset(int32_t* q, int n, hipStream_t s);
 // Packs [E][N][K] row-major weights (gate_up: w0 = gate, w1 = up) into the
 // streaming kernel's layout.
 hipError_t launch_pack(const void* w0, const void* w1, void* dst, int E, int N, int K, bool gate_up, hipStream_t s);
