@@ -2,16 +2,19 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload dsv3]
 
-A step is one moe_layer call (gate, route, dispatch, grouped expert FFN,
-shared expert on a second stream, combine) over the workload's T tokens, with
-inputs and weights already resident in HBM. By default the routed-expert
-weights are converted once, before any timing, into the packed layout of
+A step is one moe_layer call (gate, route, dispatch, grouped expert FFN with
+the shared expert, combine) over the workload's T tokens, with inputs and
+weights already resident in HBM. By default the routed-expert weights are
+converted once, before any timing, into the packed layout of
 moe_pack_weights (a load-time conversion, like reading a checkpoint); the
-weight-streaming expert GEMMs then read them. --layout rowmajor times the
-tiled GEMMs on the plain [E][I][d] weights instead. Prints ONE JSON line:
-tokens/s of the layer, the roofline of the dominant kernel pair (the grouped
-expert FFN, timed with HIP events on its own stream), and the CPU oracle
-timed on a bounded sample of the same workload as a baseline.
+weight-streaming expert GEMMs then read them, and the shared expert runs
+inside them as one more group. --layout rowmajor times the tiled GEMMs on
+the plain [E][I][d] weights instead. Prints ONE JSON line: tokens/s of the
+layer, the roofline of the dominant kernel pair (the grouped expert FFN,
+timed with HIP events on its own stream), the CPU oracle timed on a bounded
+sample of the same workload as a baseline, the per-layer time of 1, 4 and 16
+layer calls run back to back, and side measurements of the skewed-routing,
+decode-sized and Mixtral-shaped workloads (--no-extra skips these).
 """
 from __future__ import annotations
 
@@ -75,7 +78,7 @@ def measured_traffic(workload: str, layout: str):
 
 
 def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens: int = 64,
-                 ffn_only: bool = False, layout: str = "packed"):
+                 ffn_only: bool = False, layout: str = "packed", multilayer: tuple = ()):
     import numpy as np
     import torch
 
@@ -133,6 +136,30 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
         wall = time.perf_counter() - wall0
         ms = e0.elapsed_time(e1) / steps
 
+    # multi-layer steady state: L layer calls back to back on the same input
+    # and weights (feeding each output to the next layer would change the
+    # routing, hence the work, from layer to layer), each into its own output
+    ml = {}
+    if multilayer and not ffn_only:
+        outs = [torch.empty_like(out) for _ in range(max(multilayer))]
+
+        def chain(L):
+            for i in range(L):
+                moe.moe_layer(cfg, T, t["x"], t["w_router"], t["bias"], *w_ffn, *w_sh, outs[i], ws,
+                              s_main=s_main, s_aux=s_aux)
+
+        for L in multilayer:
+            chain(L)
+            reps = max(1, steps // L)
+            m0, m1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            m0.record(s_main)
+            for _ in range(reps):
+                chain(L)
+            m1.record(s_main)
+            torch.cuda.synchronize()
+            ml[L] = m0.elapsed_time(m1) / (reps * L)
+        del outs
+
     # dominant kernel pair: the grouped expert FFN, timed alone on its stream
     y = torch.empty((T * p["k"], p["d"]), dtype=cfg.torch_dtype, device="cuda")
 
@@ -158,6 +185,10 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
         layer_mfma_frac=alg["layer_flops"] / (ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12),
         ffn_gbs=alg["ffn_bytes"] / (ffn_ms / 1e3) / 1e9,
         ffn_tflops=alg["ffn_flops"] / (ffn_ms / 1e3) / 1e12,
+        # fraction of the FFN's roofline: the larger of its byte and flop floors over its time
+        ffn_roof_frac=max(alg["ffn_bytes"] / (HBM_PEAK_GBS * 1e9), alg["ffn_flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12))
+        / (ffn_ms / 1e3),
+        multilayer_ms_per_layer=ml,
     )
     if want_cpu:
         log(f"[bench] {name}: CPU oracle baseline on {cpu_tokens} tokens")
@@ -216,7 +247,7 @@ def main():
     ap.add_argument("--layout", choices=("packed", "rowmajor"), default="packed",
                     help="routed-expert weight layout (packed: converted once before timing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-extra", action="store_true", help="skip the mixtral and decode side measurements")
+    ap.add_argument("--no-extra", action="store_true", help="skip the side measurements (other workloads, multi-layer)")
     ap.add_argument("--cpu-tokens", type=int, default=64, help="tokens in the CPU-oracle baseline sample")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run 3 plain device copies of this many MiB (reference for HBM byte counters)")
@@ -247,14 +278,14 @@ def main():
         log(f"[bench] copy calibration: 3 x {n} B, {2 * 3 * n / (c0.elapsed_time(c1) / 1e3) / 1e9:.1f} GB/s")
         del src, dst
     main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_tokens,
-                            args.ffn_only, args.layout)
+                            args.ffn_only, args.layout, multilayer=() if args.no_extra else (1, 4, 16))
     if args.ffn_only:
         print(json.dumps(dict(workload=args.workload, expert_ffn_ms=main_res["ffn_ms"],
                               expert_ffn_gbs=main_res["ffn_gbs"], expert_ffn_tflops=main_res["ffn_tflops"])))
         return
     extra = {}
     if not args.no_extra:
-        for name in ("dsv3_decode", "mixtral"):
+        for name in ("dsv3_skew", "dsv3_decode", "mixtral"):
             if name == args.workload:
                 continue
             r = run_workload(name, args.steps, args.warmup, False, layout=args.layout)
@@ -262,7 +293,10 @@ def main():
                                layer_hbm_frac=round(r["layer_hbm_frac"], 4),
                                layer_mfma_frac=round(r["layer_mfma_frac"], 4),
                                expert_ffn_ms=round(r["ffn_ms"], 4), expert_ffn_gbs=round(r["ffn_gbs"], 1),
-                               expert_ffn_tflops=round(r["ffn_tflops"], 1))
+                               expert_ffn_tflops=round(r["ffn_tflops"], 1),
+                               expert_ffn_roofline_frac=round(r["ffn_roof_frac"], 4),
+                               touched_experts=r["alg"]["touched_experts"],
+                               max_over_mean_load=round(r["counts_max_over_mean"], 3), empty_experts=r["empty_experts"])
 
     r = main_res
     p = r["p"]
@@ -305,6 +339,9 @@ def main():
     }
     if "cpu" in r:
         out["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r["cpu"].items()}
+    if r["multilayer_ms_per_layer"]:
+        out["multilayer"] = {"ms_per_layer": {str(L): round(v, 4) for L, v in r["multilayer_ms_per_layer"].items()},
+                             "note": "L layer calls back to back on the same input and weights, each into its own output"}
     if extra:
         out["extra"] = extra
     print(json.dumps(out), flush=True)
