@@ -32,8 +32,11 @@ Conventions
 
 Parity status: every function here is pinned by the CPU tests (closed forms,
 brute-force enumeration on tiny inputs, special cases that reduce to a dense
-SwiGLU or a dense softmax mixture, and invariants). The layer as a whole has
-no value printed in the paper; it is pinned only through those pieces.
+SwiGLU or a dense softmax mixture, and invariants; the token quantization by
+hand-derived examples with exact power-of-two scales, its error bound and the
+quantized layer's reduction to the plain one on exactly representable
+tokens). The layer as a whole has no value printed in the paper; it is pinned
+only through those pieces.
 """
 
 from __future__ import annotations
@@ -51,6 +54,8 @@ __all__ = [
     "combine",
     "layer",
     "layer_rows",
+    "quantize_tokens",
+    "dequantize_tokens",
 ]
 
 
@@ -278,6 +283,39 @@ def expert_ffn(x, sorted_token, offsets, w_gate, w_up, w_down) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
+# token quantization around the dispatch exchange (App. F pipeline: quantize
+# tokens to int8 with per-token scales, send, dequantize before GEMM1; App. M
+# steps (1)-(3))
+# ---------------------------------------------------------------------------
+
+def quantize_tokens(x):
+    """Per-token symmetric int8 quantization of the token rows.
+
+    ``scale[t] = max_c |x[t, c]| / 127`` and ``codes[t, c] = x[t, c] / scale[t]``
+    rounded half to even and clamped to [-127, 127]; a row of zeros gets scale
+    0 and codes 0. The paper fixes int8 codes and one scale per token but no
+    precision; because the divisions decide integers, they run in float32 (the
+    kernel's precision), on the same float32 inputs the kernel reads. Returns
+    (codes int8 [T, d], scales float32 [T]).
+    """
+    xf = to_f64(x).astype(np.float32)  # bf16 and fp32 inputs are exact in float32
+    if xf.ndim != 2:
+        raise ValueError("x must be [T, d]")
+    absmax = np.abs(xf).max(axis=1) if xf.shape[1] else np.zeros(xf.shape[0], np.float32)
+    scales = (absmax / np.float32(127.0)).astype(np.float32)
+    safe = np.where(scales > 0, scales, np.float32(1.0)).astype(np.float32)
+    q = np.rint(xf / safe[:, None])  # float32 division, round half to even
+    q = np.clip(q, -127, 127)
+    q[scales == 0] = 0
+    return q.astype(np.int8), scales
+
+
+def dequantize_tokens(codes, scales) -> np.ndarray:
+    """``codes[t, c] * scales[t]`` in fp64 (the tokens GEMM1 sees)."""
+    return np.asarray(codes, dtype=np.float64) * np.asarray(scales, dtype=np.float64)[:, None]
+
+
+# ---------------------------------------------------------------------------
 # combine: the single-GPU form of the reverse all-to-all
 # ---------------------------------------------------------------------------
 
@@ -314,16 +352,21 @@ def layer(cfg: dict, x, w_router, bias, w_gate, w_up, w_down,
     """The full layer: gate, route, dispatch, expert FFN, shared expert, combine.
 
     cfg holds ``E, k, score, n_groups, topk_groups, renorm, scale`` and
-    ``n_shared`` (0 or 1). ``logits`` replaces the gate when given (used to
-    re-route from logits computed elsewhere). The shared-expert weights are
-    [I_s, d], [I_s, d] and [d, I_s]. Returns every intermediate.
+    ``n_shared`` (0 or 1), and optionally ``quant`` ("int8": the routed
+    experts see the tokens after :func:`quantize_tokens` and
+    :func:`dequantize_tokens`; the gate and the shared expert, which stay on
+    the sending side in the paper's pipeline, see the original tokens).
+    ``logits`` replaces the gate when given (used to re-route from logits
+    computed elsewhere). The shared-expert weights are [I_s, d], [I_s, d] and
+    [d, I_s]. Returns every intermediate.
     """
     if logits is None:
         logits = gate_logits(x, w_router)
     rb = None if cfg["score"] == "softmax" else bias
     topk_idx, topk_w, det = route(logits, bias=rb, return_detail=True, **_route_kwargs(cfg))
     counts, offsets, sorted_token, sorted_assign, inv_perm = dispatch(topk_idx, cfg["E"])
-    y_perm = expert_ffn(x, sorted_token, offsets, w_gate, w_up, w_down)
+    x_routed = dequantize_tokens(*quantize_tokens(x)) if cfg.get("quant") == "int8" else x
+    y_perm = expert_ffn(x_routed, sorted_token, offsets, w_gate, w_up, w_down)
     shared = None
     if cfg.get("n_shared", 0):
         shared = swiglu_ffn(x, ws_gate, ws_up, ws_down)
@@ -335,7 +378,7 @@ def layer(cfg: dict, x, w_router, bias, w_gate, w_up, w_down,
 
 
 def layer_rows(x, rows, topk_idx, topk_w, w_gate, w_up, w_down,
-               ws_gate=None, ws_up=None, ws_down=None) -> np.ndarray:
+               ws_gate=None, ws_up=None, ws_down=None, quant=None) -> np.ndarray:
     """Layer outputs for a subset of tokens, given their routing.
 
     The FFN acts on each row independently, so ``out[t]`` needs only token
@@ -343,16 +386,20 @@ def layer_rows(x, rows, topk_idx, topk_w, w_gate, w_up, w_down,
     ``out[t] = sum_j topk_w[t, j] * FFN_{topk_idx[t, j]}(x[t]) (+ shared(x[t]))``.
     rows: token indices; ``topk_idx``/``topk_w``: [len(rows), k] for those
     tokens. Experts are visited once each, so a large resident weight tensor
-    is decoded one expert at a time. Returns [len(rows), d] in fp64.
+    is decoded one expert at a time. ``quant="int8"``: the routed experts see
+    the quantized tokens (the quantization is per token, so a subset of rows
+    quantizes as it would inside the whole batch). Returns [len(rows), d] in
+    fp64.
     """
     X = to_f64(np.asarray(x)[np.asarray(rows, dtype=np.int64)])
+    Xr = dequantize_tokens(*quantize_tokens(np.asarray(x)[np.asarray(rows, dtype=np.int64)])) if quant == "int8" else X
     idx = np.asarray(topk_idx, dtype=np.int64)
     W = np.asarray(topk_w, dtype=np.float64)
     R, k = idx.shape
     y = np.zeros((R, k, X.shape[1]))
     for e in np.unique(idx):
         sel_r, sel_j = np.nonzero(idx == e)
-        y[sel_r, sel_j] = swiglu_ffn(X[sel_r], w_gate[e], w_up[e], w_down[e])
+        y[sel_r, sel_j] = swiglu_ffn(Xr[sel_r], w_gate[e], w_up[e], w_down[e])
     out = np.zeros((R, X.shape[1]))
     for j in range(k):
         out += W[:, j : j + 1] * y[:, j]

@@ -429,3 +429,107 @@ def test_max_rel_err_metric():
     rms = math.sqrt((1 + 4 + 0 + 16) / 4)
     got = want + np.array([0.01, 0.0, 0.05, 0.0])
     assert max_rel_err(got, want) == pytest.approx(max(0.01 / rms, 0.05 / rms))
+
+
+# ---------------------------------------------------------------------------
+# token quantization (App. F pipeline: int8 codes, one scale per token)
+# ---------------------------------------------------------------------------
+
+def _bf16_bits(a):
+    """float32 values that bf16 represents exactly -> their bf16 bit patterns."""
+    b = np.asarray(a, dtype=np.float32).view(np.uint32)
+    assert (b & 0xFFFF == 0).all(), "value not exact in bf16"
+    return (b >> 16).astype(np.uint16)
+
+
+def test_quantize_worked_examples():
+    ex = json.load(open(os.path.join(GOLDEN, "quant_examples.json")))
+    for name in ("Q1", "Q2", "Q3", "Q4"):
+        e = ex[name]
+        for x in (np.asarray([e["x"]], np.float32), _bf16_bits([e["x"]])):
+            codes, scales = O.quantize_tokens(x)
+            assert codes.dtype == np.int8 and scales.dtype == np.float32
+            assert codes[0].tolist() == e["codes"], name
+            assert float(scales[0]) == e["scale"], name
+
+
+def test_quantize_invariants_and_error_bound():
+    rng = np.random.default_rng(7)
+    x = (rng.standard_normal((64, 300)) * rng.uniform(0.01, 50, (64, 1))).astype(np.float32)
+    x[3] = 0.0
+    codes, scales = O.quantize_tokens(x)
+    assert np.abs(codes.astype(np.int32)).max() <= 127
+    nz = scales > 0
+    # the largest |x| of every non-zero row maps to +-127
+    assert (np.abs(codes[nz].astype(np.int32)).max(axis=1) == 127).all()
+    assert scales[3] == 0 and (codes[3] == 0).all()
+    # scale is max|x|/127 to float32 rounding
+    np.testing.assert_allclose(scales[nz], np.abs(x[nz]).max(axis=1) / 127.0, rtol=2 ** -23)
+    # round to nearest: every element within half a step (plus float32 rounding)
+    err = np.abs(O.dequantize_tokens(codes, scales) - x)
+    assert (err <= scales[:, None] * (0.5 + 2 ** -20) + 1e-30).all()
+    # a power-of-two rescaling of a row changes only its scale
+    c2, s2 = O.quantize_tokens(x * np.float32(8.0))
+    assert np.array_equal(c2, codes) and np.array_equal(s2, scales * np.float32(8.0))
+    # per token: quantizing a subset of rows gives the same rows
+    c3, s3 = O.quantize_tokens(x[10:20])
+    assert np.array_equal(c3, codes[10:20]) and np.array_equal(s3, scales[10:20])
+
+
+def test_quantize_rounding_is_half_even_not_half_away():
+    # max |x| = 127 gives scale 1: ties at .5 go to the even integer
+    x = np.asarray([[127.0, 0.5, 1.5, 2.5, -1.5, -126.5]], np.float32)
+    codes, _ = O.quantize_tokens(x)
+    assert codes[0].tolist() == [127, 0, 2, 2, -2, -126]
+
+
+def test_quantize_bound_catches_planted_off_by_one():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((8, 64)).astype(np.float32)
+    codes, scales = O.quantize_tokens(x)
+    bad = codes.copy()
+    frac = np.abs(x[2] / scales[2]) % 1
+    r, c = 2, int(np.argmax(np.abs(frac - 0.5)))  # the element farthest from a rounding tie
+    bad[r, c] += 1 if bad[r, c] < 127 else -1
+    err = np.abs(O.dequantize_tokens(bad, scales) - x)
+    assert (err > scales[:, None] * (0.5 + 2 ** -20)).any()
+
+
+def test_quantized_layer_equals_plain_layer_on_exact_tokens():
+    # tokens that are integers times max|x|/127 (a power of two) survive the
+    # quantization exactly, so the quantized layer is the plain layer
+    rng = np.random.default_rng(11)
+    T, d, E, I = 20, 32, 4, 16
+    x = (rng.integers(-127, 128, (T, d)).astype(np.float32) * np.float32(0.25))
+    x[:, 0] = 127 * 0.25
+    wr = rng.standard_normal((E, d)) * 0.1
+    wg, wu = rng.standard_normal((E, I, d)) * 0.2, rng.standard_normal((E, I, d)) * 0.2
+    wd = rng.standard_normal((E, d, I)) * 0.2
+    cfg = dict(E=E, k=2, score="softmax", n_groups=1, topk_groups=1, renorm=True, scale=1.0, n_shared=0)
+    a = O.layer(cfg, x, wr, None, wg, wu, wd)
+    b = O.layer(dict(cfg, quant="int8"), x, wr, None, wg, wu, wd)
+    assert np.array_equal(a["out"], b["out"])
+    # and a non-exact token changes it, by no more than the quantization step allows
+    x2 = x.copy()
+    x2[5, 3] += np.float32(0.1)
+    c = O.layer(dict(cfg, quant="int8"), x2, wr, None, wg, wu, wd)
+    d_ = O.layer(cfg, x2, wr, None, wg, wu, wd)
+    assert not np.array_equal(c["out"], d_["out"])
+    assert max_rel_err(c["out"], d_["out"]) < 0.05
+
+
+def test_layer_rows_quantized_agrees_with_full_layer():
+    rng = np.random.default_rng(12)
+    T, d, E, I = 24, 64, 8, 16
+    x = rng.standard_normal((T, d)).astype(np.float32)
+    wr = rng.standard_normal((E, d)) * 0.1
+    wg, wu = rng.standard_normal((E, I, d)) * 0.2, rng.standard_normal((E, I, d)) * 0.2
+    wd = rng.standard_normal((E, d, I)) * 0.2
+    sg, su, sd = rng.standard_normal((I, d)) * 0.2, rng.standard_normal((I, d)) * 0.2, rng.standard_normal((d, I)) * 0.2
+    cfg = dict(E=E, k=3, score="sigmoid", n_groups=4, topk_groups=2, renorm=True, scale=2.5, n_shared=1,
+               quant="int8")
+    bias = np.zeros(E)
+    full = O.layer(cfg, x, wr, bias, wg, wu, wd, sg, su, sd)
+    rows = np.array([0, 5, 23])
+    part = O.layer_rows(x, rows, full["topk_idx"][rows], full["topk_w"][rows], wg, wu, wd, sg, su, sd, quant="int8")
+    np.testing.assert_allclose(part, full["out"][rows], rtol=1e-12, atol=1e-12)
