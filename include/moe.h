@@ -84,6 +84,15 @@ typedef enum {
                               T*d and T*k*I below 2^31 elements                               */
 } moe_layout_t;
 
+/* Compression of the tokens the routed experts receive (App. F pipeline:
+ * quantize before the dispatch exchange, dequantize before GEMM1). */
+typedef enum {
+  MOE_QUANT_NONE = 0, /* the routed experts see the bf16/fp32 tokens                */
+  MOE_QUANT_INT8 = 1  /* int8 codes with one fp32 scale per token (moe_quantize);
+                         bf16 and MOE_LAYOUT_PACKED only; the gate and the shared
+                         expert, on the sending side, keep the original tokens       */
+} moe_quant_t;
+
 typedef struct {
   int32_t d;           /* hidden size                                         */
   int32_t E;           /* routed experts                                      */
@@ -98,6 +107,7 @@ typedef struct {
   float route_scale;   /* multiplies every weight (1.0 Mixtral, 2.5 DSV3)     */
   int32_t dtype;       /* moe_dtype_t                                         */
   int32_t weight_layout; /* moe_layout_t of the routed-expert weights          */
+  int32_t token_quant;   /* moe_quant_t of the routed experts' input tokens    */
 } moe_config_t;
 
 /* Optional device buffers moe_layer writes its intermediates into (each may be
@@ -177,6 +187,35 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x,
                    size_t ws_bytes, hipStream_t stream);
 
 /*
+ * moe_quantize — per-token int8 quantization of the tokens (App. F pipeline,
+ * the step before the dispatch exchange; App. M step (1)):
+ *   scale[t]    = max_c |x[t][c]| / 127                       (fp32)
+ *   codes[t][c] = x[t][c] / scale[t] in fp32, rounded half to even,
+ *                 clamped to [-127, 127]; a zero row: scale 0, codes 0.
+ *  x : [T][d] bf16 (cfg->dtype must be MOE_BF16).
+ *  codes : [T][d] int8 out.   scales : [T] fp32 out.
+ */
+int moe_quantize(const moe_config_t* cfg, int32_t T, const void* x, int8_t* codes, float* scales,
+                 hipStream_t stream);
+
+/*
+ * moe_expert_ffn_q8 — moe_expert_ffn on quantized tokens (App. M step (3):
+ * dequantize + GEMM1 + SwiGLU + GEMM2): for every expert e and row r,
+ *   t = sorted_token[r], h[r] = silu(s_t q_t · w_gate[e]ᵀ) * (s_t q_t · w_up[e]ᵀ),
+ *   y_perm[r] = h[r] · w_down[e]ᵀ
+ * with q_t = codes[t], s_t = scales[t]. The dequantization is fused into
+ * GEMM1: the gathered code rows are converted to bf16 (exactly) as they are
+ * loaded, and each row's sums are multiplied by its scale before the SwiGLU.
+ * Packed weights only (cfg->weight_layout == MOE_LAYOUT_PACKED, bf16).
+ *  codes : [T][d] int8, scales : [T] fp32 (from moe_quantize).
+ *  w_gate_up, w_down : packed weights from moe_pack_weights.
+ *  y_perm : [T*k][d] bf16 out.
+ */
+int moe_expert_ffn_q8(const moe_config_t* cfg, int32_t T, const int8_t* codes, const float* scales,
+                      const int32_t* sorted_token, const int32_t* offsets, const void* w_gate_up,
+                      const void* w_down, void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * moe_shared_ffn — the shared expert: the same SwiGLU FFN, with intermediate
  * size cfg->I_shared, applied to all T tokens (dense, unweighted).
  *  ws_gate, ws_up, ws_down : row-major, or with MOE_LAYOUT_PACKED the output
@@ -213,6 +252,10 @@ int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const in
  *           it is computed inside the routed expert GEMMs as one more group
  *           (its compute fills the matrix cores of the memory-bound routed
  *           work); the result is the same.
+ *           With cfg->token_quant == MOE_QUANT_INT8 the tokens are quantized
+ *           first (moe_quantize, into the workspace) and the routed experts
+ *           run on the codes (moe_expert_ffn_q8); the gate and the shared
+ *           expert use x, and the shared expert is then not fused.
  *  out    : [T][d] dtype out.
  *  dbg    : NULL, or device buffers to receive intermediates (see above).
  * On return, s_main carries all the work (s_aux is joined into it).

@@ -52,7 +52,7 @@ constexpr int kQueueInts = 32;
 // Byte offsets of every scratch region inside the caller's workspace.
 struct Layout {
   size_t gate_partials, logits, topk_idx, topk_w, masks, bases, counts, offsets, sorted_token, sorted_assign,
-      inv_perm, h, y_perm, shared_h, shared_out, queues, total;
+      inv_perm, h, y_perm, shared_h, shared_out, queues, qcodes, qscales, total;
 };
 
 Layout make_layout(const moe_config_t& c, int32_t T) {
@@ -82,6 +82,9 @@ Layout make_layout(const moe_config_t& c, int32_t T) {
   L.shared_h = take(c.n_shared ? t * c.I_shared * es : 0);
   L.shared_out = take(c.n_shared ? t * c.d * es : 0);
   L.queues = take(kQueueInts * 4);
+  const bool q8 = c.token_quant == MOE_QUANT_INT8;
+  L.qcodes = take(q8 ? t * c.d : 0);  // moe_layer's quantized tokens
+  L.qscales = take(q8 ? t * 4 : 0);
   L.total = off;
   return L;
 }
@@ -113,6 +116,10 @@ int validate(const moe_config_t* c, int32_t T) {
   if ((int64_t)T * c->k >= (int64_t)1 << 31) return fail(MOE_ERR_UNSUPPORTED, "T*k >= 2^31");
   if (c->weight_layout != MOE_LAYOUT_ROWMAJOR && c->weight_layout != MOE_LAYOUT_PACKED)
     return fail(MOE_ERR_INVALID_ARG, "unknown weight layout");
+  if (c->token_quant != MOE_QUANT_NONE && c->token_quant != MOE_QUANT_INT8)
+    return fail(MOE_ERR_INVALID_ARG, "unknown token quantization");
+  if (c->token_quant == MOE_QUANT_INT8 && (c->dtype != MOE_BF16 || c->weight_layout != MOE_LAYOUT_PACKED))
+    return fail(MOE_ERR_UNSUPPORTED, "int8 tokens need bf16 and packed weights");
   if (c->weight_layout == MOE_LAYOUT_PACKED &&
       (c->dtype != MOE_BF16 || c->I % 128 != 0 || c->d % 256 != 0 || (c->n_shared && c->I_shared % 128 != 0)))
     return fail(MOE_ERR_UNSUPPORTED, "packed weights need bf16, I and I_shared % 128 == 0 and d % 256 == 0");
@@ -231,10 +238,11 @@ struct FusedShared {
 // the weight-streaming kernel; fused (packed only, same intermediate size):
 // the shared expert over all a_rows tokens rides along as an extra group.
 // queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path.
+// x_scales: x holds int8 codes of rows with these fp32 scales (packed only).
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
-                   int32_t* queues = nullptr) {
+                   int32_t* queues = nullptr, const float* x_scales = nullptr) {
   if (packed && queues) {
     const hipError_t e = moe::launch_queue_reset(queues, 16, s);
     if (e != hipSuccess) return e;
@@ -259,6 +267,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
     up.x_rows = a_rows;
   }
   up.tile_queue = queues;
+  up.a_scale = x_scales;
   hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
   if (e != hipSuccess) return e;
   moe::GemmProblem down{};
@@ -404,6 +413,40 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
 }
 
+int moe_quantize(const moe_config_t* cfg, int32_t T, const void* x, int8_t* codes, float* scales,
+                 hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  if (cfg->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "moe_quantize needs bf16 tokens");
+  MOE_CHECK(need(x, "x"));
+  MOE_CHECK(need(codes, "codes"));
+  MOE_CHECK(need(scales, "scales"));
+  if (T == 0) return MOE_OK;
+  const hipError_t e = moe::launch_quantize(x, codes, scales, T, cfg->d, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "quantize");
+}
+
+int moe_expert_ffn_q8(const moe_config_t* cfg, int32_t T, const int8_t* codes, const float* scales,
+                      const int32_t* sorted_token, const int32_t* offsets, const void* w_gate_up,
+                      const void* w_down, void* y_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  if (cfg->dtype != MOE_BF16 || cfg->weight_layout != MOE_LAYOUT_PACKED)
+    return fail(MOE_ERR_UNSUPPORTED, "moe_expert_ffn_q8 needs bf16 and packed weights");
+  MOE_CHECK(need(codes, "codes"));
+  MOE_CHECK(need(scales, "scales"));
+  MOE_CHECK(need(sorted_token, "sorted_token"));
+  MOE_CHECK(need(offsets, "offsets"));
+  MOE_CHECK(need(w_gate_up, "w_gate_up"));
+  MOE_CHECK(need(w_down, "w_down"));
+  MOE_CHECK(need(y_perm, "y_perm"));
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  if (T == 0) return MOE_OK;
+  const Layout L = make_layout(*cfg, T);
+  const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, codes, sorted_token, offsets, w_gate_up, nullptr,
+                               w_down, static_cast<char*>(ws) + L.h, y_perm, stream, true, nullptr,
+                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), scales);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN (int8 tokens)");
+}
+
 int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void* ws_gate, const void* ws_up,
                    const void* ws_down, void* out, void* ws, size_t ws_bytes, hipStream_t stream) {
   MOE_CHECK(validate(cfg, T));
@@ -483,7 +526,8 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   // inside the routed expert GEMMs as one more group, so its compute fills
   // the matrix cores of the memory-bound routed work. Otherwise it runs on
   // its own, on s_aux when given (overlapping gate, routing and dispatch).
-  const bool fuse = packed && c.n_shared && c.I_shared == c.I;
+  const bool q8 = c.token_quant == MOE_QUANT_INT8;
+  const bool fuse = packed && c.n_shared && c.I_shared == c.I && !q8;
   const bool two = c.n_shared && !fuse && s_aux && s_aux != s_main;
   StreamEvents* ev = nullptr;
   if (two) {
@@ -501,6 +545,10 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     return hip_fail(e, "route");
   if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main)) != hipSuccess)
     return hip_fail(e, "dispatch");
+  int8_t* const qcodes = reinterpret_cast<int8_t*>(w + L.qcodes);
+  float* const qscales = reinterpret_cast<float*>(w + L.qscales);
+  if (q8 && (e = moe::launch_quantize(x, qcodes, qscales, T, c.d, s_main)) != hipSuccess)
+    return hip_fail(e, "quantize");
   FusedShared fs;
   if (fuse) {
     fs.w_gate_up = ws_gate;
@@ -508,8 +556,9 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     fs.h = w + L.shared_h;
     fs.out = shared;
   }
-  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, x, st, offsets, w_gate, w_up, w_down, w + L.h, y, s_main, packed,
-                   fuse ? &fs : nullptr, queues)) != hipSuccess)
+  if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
+                   w_down, w + L.h, y, s_main, packed, fuse ? &fs : nullptr, queues, q8 ? qscales : nullptr)) !=
+      hipSuccess)
     return hip_fail(e, "expert FFN");
   if (c.n_shared && !fuse) {
     if (two) {

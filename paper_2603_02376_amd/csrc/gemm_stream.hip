@@ -81,6 +81,24 @@ __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "m
 __device__ __forceinline__ int lds_off(int row, int chunk) { return (row << 7) + ((chunk ^ ((row >> 1) & 7)) << 4); }
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+// 16 int8 codes (one 16-byte load, element e in byte e) -> the same 16 values
+// as bf16 in two 16-byte chunks (elements 0-7, 8-15). Integers of at most 8
+// bits are exact in bf16, so keeping the high half of the fp32 value is exact.
+__device__ __forceinline__ void codes_to_bf16(i32x4 v, i32x4& lo, i32x4& hi) {
+  uint32_t o[8];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    float f[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) f[j] = (float)(int)__builtin_amdgcn_sbfe(v[d], 8 * j, 8);  // sign-extended byte j
+    // bytes 2,3 of the first value, then bytes 2,3 of the second
+    o[2 * d] = __builtin_amdgcn_perm(__float_as_uint(f[1]), __float_as_uint(f[0]), 0x07060302u);
+    o[2 * d + 1] = __builtin_amdgcn_perm(__float_as_uint(f[3]), __float_as_uint(f[2]), 0x07060302u);
+  }
+  lo = i32x4{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+  hi = i32x4{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+}
+
 template <typename F, int... Is>
 __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
   (f(std::integral_constant<int, Is>{}), ...);
@@ -100,7 +118,7 @@ __device__ __forceinline__ void with_count(int n, F&& f) {
   }
 }
 
-__device__ int scan4(int v, int* scratch, int* total) {
+__device__ __forceinline__ int scan4(int v, int* scratch, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int inc = v;
 #pragma unroll
@@ -123,7 +141,7 @@ __device__ int scan4(int v, int* scratch, int* total) {
 
 // EPI_SWIGLU: GEMM1 (j = gate/up, 32 output columns per wave);
 // EPI_STORE:  GEMM2 (j = two 32-column halves, 64 output columns per wave).
-template <int EPI>
+template <int EPI, bool Q8>
 __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
   constexpr int WCOLS = (EPI == EPI_SWIGLU) ? 32 : 64;  // output columns per wave
   constexpr int TCOLS = WCOLS * kWaves;                  // per tile
@@ -131,6 +149,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int tstart[257];
   __shared__ int scan_scratch[kWaves];
+  __shared__ float s_scale[kMaxRows];  // Q8: the tile's row scales
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int groups = p.offsets ? p.groups : 1;
@@ -180,6 +199,10 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   // + 0..7): lane l carries row l/8 of the block and the logical 16-byte chunk
   // that lds_off() places at physical chunk l%8.
   const int lr = lane >> 3, lc = (lane & 7) ^ ((wave * 4 + (lr >> 1)) & 7);
+  // Q8: A rows of int8 codes move in 1 KB blocks of 16 rows of 64 bytes
+  // (block i of a wave: rows 64 i + 16 wave + 0..15): lane l carries row l/4
+  // and codes 16 (l%4) .. 16 (l%4) + 15 of the step's 64.
+  const int lr8 = lane >> 2, lc8 = lane & 3;
 
   for (int tile = vb; tile < total_tiles;) {
     // claim the next entry of this XCD's queue now; it is used after this tile
@@ -238,7 +261,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       c_base = static_cast<__bf16*>(p.C);
     }
     const __amdgpu_buffer_rsrc_t a_rs = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<void*>(a_base), (short)0, (int)(uint32_t)((size_t)a_rows * K * 2), 0x00020000);
+        const_cast<void*>(a_base), (short)0, (int)(uint32_t)((size_t)a_rows * K * (Q8 ? 1 : 2)), 0x00020000);
 
     // this wave's packed weights: contiguous nk * 32 KB per tile, 8 KB per wave per step
     const char* bw = b_base + (size_t)wave * kStepBytes + lane * 16;
@@ -252,16 +275,30 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     const int nact = __builtin_amdgcn_readfirstlane((rows + 31) / 32);
 
-    auto body = [&](auto ar_c) {
+    auto body = [&](auto ar_c) __attribute__((always_inline)) {
       constexpr int AR = decltype(ar_c)::value;  // A rows staged per step (128 or kMaxRows)
-      constexpr int A_CH = AR / (8 * kWaves);
+      constexpr int A_CH = Q8 ? AR / (16 * kWaves) : AR / (8 * kWaves);  // A loads per wave per step
       constexpr int LOADS = A_CH + 8;
       uint32_t a_off[A_CH];  // byte offsets into A (its size is checked below 4 GiB at launch)
 #pragma unroll
       for (int i = 0; i < A_CH; ++i) {
-        const int r = min(i * 8 * kWaves + wave * 8 + lr, rows - 1);
-        const int ar = gather ? min(max(gather[row0 + r], 0), a_rows - 1) : row0 + r;
-        a_off[i] = (uint32_t)ar * (uint32_t)(K * 2) + lc * 16;
+        if constexpr (Q8) {
+          const int r = min(i * 16 * kWaves + wave * 16 + lr8, rows - 1);
+          const int ar = gather ? min(max(gather[row0 + r], 0), a_rows - 1) : row0 + r;
+          a_off[i] = (uint32_t)ar * (uint32_t)K + lc8 * 16;
+        } else {
+          const int r = min(i * 8 * kWaves + wave * 8 + lr, rows - 1);
+          const int ar = gather ? min(max(gather[row0 + r], 0), a_rows - 1) : row0 + r;
+          a_off[i] = (uint32_t)ar * (uint32_t)(K * 2) + lc * 16;
+        }
+      }
+      // Q8: the scale of tile row tid, written to s_scale before the K loop
+      float row_scale = 0.f;
+      if constexpr (Q8) {
+        if (tid < rows) {
+          const int ar = gather ? min(max(gather[row0 + tid], 0), a_rows - 1) : row0 + tid;
+          row_scale = p.a_scale[ar];
+        }
       }
       // Per wave, in flight: weights for kDepth-1 steps ahead (kDepth register
       // sets) and its share of the A rows of the steps two and three ahead
@@ -272,27 +309,41 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       i32x4 sa[kStage][A_CH];
       // Steps past the end are clamped to the last one: those surplus loads
       // are never used, which keeps the steady-state loop free of branches.
-      auto load_a = [&](int ks, auto s_c, int i) {
+      auto load_a = [&](int ks, auto s_c, int i) __attribute__((always_inline)) {
         const int kc = min(ks, nk - 1);
-        sa[decltype(s_c)::value][i] = __builtin_amdgcn_raw_buffer_load_b128(a_rs, (int)(a_off[i] + kc * 128), 0, 0);
+        sa[decltype(s_c)::value][i] =
+            __builtin_amdgcn_raw_buffer_load_b128(a_rs, (int)(a_off[i] + kc * (Q8 ? 64 : 128)), 0, 0);
       };
-      auto load_b = [&](int ks, auto s_c, int n) {
+      auto load_b = [&](int ks, auto s_c, int n) __attribute__((always_inline)) {
         const int kc = min(ks, nk - 1);
         bq[decltype(s_c)::value][n] = __builtin_nontemporal_load(
             reinterpret_cast<const i32x4*>(bw + (size_t)kc * kWaves * kStepBytes + n * 1024));
       };
       // Write A register set S into ring slot R (layout of lds_off(): lane l
-      // holds row l/8 of each 8-row block, at physical chunk l%8).
-      auto stage = [&](auto s_c, auto r_c) {
-        char* const dst = smem + decltype(r_c)::value * (kMaxRows * 128) + wave * 8 * 128 + lane * 16;
+      // holds row l/8 of each 8-row block, at physical chunk l%8). Q8: each
+      // lane's 16 codes become the row's bf16 chunks 2 (l%4) and 2 (l%4) + 1.
+      auto stage = [&](auto s_c, auto r_c) __attribute__((always_inline)) {
+        if constexpr (Q8) {
+          char* const slot = smem + decltype(r_c)::value * (kMaxRows * 128);
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i)
-          *reinterpret_cast<i32x4*>(dst + i * 8 * kWaves * 128) = sa[decltype(s_c)::value][i];
+          for (int i = 0; i < A_CH; ++i) {
+            const int r = i * 16 * kWaves + wave * 16 + lr8;
+            i32x4 lo, hi;
+            codes_to_bf16(sa[decltype(s_c)::value][i], lo, hi);
+            *reinterpret_cast<i32x4*>(slot + lds_off(r, 2 * lc8)) = lo;
+            *reinterpret_cast<i32x4*>(slot + lds_off(r, 2 * lc8 + 1)) = hi;
+          }
+        } else {
+          char* const dst = smem + decltype(r_c)::value * (kMaxRows * 128) + wave * 8 * 128 + lane * 16;
+#pragma unroll
+          for (int i = 0; i < A_CH; ++i)
+            *reinterpret_cast<i32x4*>(dst + i * 8 * kWaves * 128) = sa[decltype(s_c)::value][i];
+        }
       };
 
-      auto kloop = [&](auto nact_c) {
+      auto kloop = [&](auto nact_c) __attribute__((always_inline)) {
         constexpr int NACT = decltype(nact_c)::value;
-        auto rd = [&](int slot, int kk, int i) {
+        auto rd = [&](int slot, int kk, int i) __attribute__((always_inline)) {
           return *reinterpret_cast<const i32x4*>(smem + slot * (kMaxRows * 128) +
                                                  lds_off(32 * i + (lane & 31), 2 * kk + (lane >> 5)));
         };
@@ -307,7 +358,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         // TAIL: one of the last steps, whose loads past the last K step are
         // skipped (elsewhere every load is in range, and the loads stay
         // unconditional so the compiler's wait counts are exact).
-        auto step = [&](int ks, auto u_c, auto tail_c) {
+        auto step = [&](int ks, auto u_c, auto tail_c) __attribute__((always_inline)) {
           constexpr int U = decltype(u_c)::value;
           constexpr bool TAIL = decltype(tail_c)::value;
           const bool a_ok = !TAIL || ks + 3 < nk, b_ok = !TAIL || ks + kDepth - 1 < nk;
@@ -372,6 +423,9 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         });
         stage(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
         stage(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{});
+        if constexpr (Q8) {
+          if (tid < kMaxRows) s_scale[tid] = row_scale;  // published by the barrier below
+        }
         // step 2's rows take set 0 (free again); step 0 then loads step 3's
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) load_a(2, std::integral_constant<int, 0>{}, i);
@@ -417,7 +471,11 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
             if (EPI == EPI_SWIGLU) {
               bf16x4 v;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = static_cast<__bf16>(silu_f(acc[i][0][4 * g + e]) * acc[i][1][4 * g + e]);
+              for (int e = 0; e < 4; ++e) {
+                // Q8: the sums ran over the codes; the row's scale restores the tokens
+                const float sc = Q8 ? s_scale[r] : 1.0f;
+                v[e] = static_cast<__bf16>(silu_f(acc[i][0][4 * g + e] * sc) * (acc[i][1][4 * g + e] * sc));
+              }
               const int c = wave * 4 + g;
               *reinterpret_cast<bf16x4*>(orow + ((c ^ (r & 7)) << 4) + 8 * h) = v;
             } else {
@@ -505,9 +563,9 @@ __global__ void pack_kernel(const __bf16* __restrict__ w0, const __bf16* __restr
   }
 }
 
-template <int EPI>
+template <int EPI, bool Q8>
 hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
-  auto kern = gemm_stream_kernel<EPI>;
+  auto kern = gemm_stream_kernel<EPI, Q8>;
   // the A ring, reused after each tile's K loop as the LDS copy of its output
   constexpr size_t lds = std::max<size_t>((size_t)kSlots * kMaxRows * 128,
                                           (size_t)kMaxRows * ((EPI == EPI_SWIGLU) ? 128 : 256) * 2);
@@ -518,8 +576,9 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
   });
   if (init_err != hipSuccess) return init_err;
   // A is addressed through a buffer resource: 32-bit byte offsets.
-  if ((size_t)p.a_rows * (size_t)p.K * 2 > 0xFFFFFFFFull || (size_t)p.x_rows * (size_t)p.K * 2 > 0xFFFFFFFFull)
+  if ((size_t)p.a_rows * (size_t)p.K * (Q8 ? 1 : 2) > 0xFFFFFFFFull || (size_t)p.x_rows * (size_t)p.K * 2 > 0xFFFFFFFFull)
     return hipErrorInvalidValue;
+  if (Q8 && (p.x_rows != 0 || !p.a_scale)) return hipErrorInvalidValue;
   if (p.x_rows < 0 || (p.x_rows > 0 && (!p.xA || !p.xB || !p.xC))) return hipErrorInvalidValue;
   const int tcols = (EPI == EPI_SWIGLU) ? 128 : 256;
   const int groups = p.offsets ? p.groups : 1;
@@ -538,8 +597,9 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
 
 hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
   if ((p.M <= 0 && p.x_rows <= 0) || p.N <= 0) return hipSuccess;
-  if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU>(p, s);
-  return launch_stream<EPI_STORE>(p, s);
+  if (p.a_scale) return epi == EPI_SWIGLU ? launch_stream<EPI_SWIGLU, true>(p, s) : hipErrorInvalidValue;
+  if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU, false>(p, s);
+  return launch_stream<EPI_STORE, false>(p, s);
 }
 
 hipError_t launch_queue_reset(int32_t* q, int n, hipStream_t s) {

@@ -63,6 +63,11 @@ struct GemmProblem {
   // launch, from which workgroups claim tiles after their first (nullptr:
   // a static round-robin schedule).
   int32_t* tile_queue;
+  // Weight-streaming kernel, EPI_SWIGLU only: A holds int8 codes ([*][K]
+  // bytes) of rows whose fp32 scales are a_scale[A row]; every output row's
+  // gate and up sums are multiplied by its row's scale before the SwiGLU.
+  // The extra group must be empty (x_rows == 0). nullptr: A is bf16.
+  const float* a_scale;
 };
 
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
@@ -121,6 +126,11 @@ struct CombineParams {
   int32_t T, k, d;
 };
 hipError_t launch_combine(const CombineParams& p, bool bf16, hipStream_t s);
+
+// Per-token int8 quantization: codes[t][c] = rne(x[t][c] / scale[t]) clamped
+// to +-127, scale[t] = max_c |x[t][c]| / 127 (0 and codes 0 for a zero row).
+// x bf16 [T][d], d % 64 == 0; codes int8 [T][d]; scales fp32 [T].
+hipError_t launch_quantize(const void* x, int8_t* codes, float* scales, int T, int d, hipStream_t s);
 
 // Number of compute units of the current device (cached per device).
 int device_cu_count();

@@ -1,0 +1,71 @@
+// Per-token int8 quantization of the token rows (the pipeline of App. F
+// quantizes the tokens to int8 with one scale per token before the dispatch
+// exchange and dequantizes them on the expert side before GEMM1).
+//
+//   scale[t]    = max_c |x[t, c]| / 127           (fp32, IEEE division)
+//   codes[t, c] = rne(x[t, c] / scale[t])         (fp32 division, round half
+//                                                  to even, clamped to +-127)
+// A row of zeros gets scale 0 and codes 0. One wave per token row: each lane
+// reads 8 bf16 (16 bytes) at a time, the wave reduces the row's maximum with
+// butterfly shuffles, then every lane writes its 8 codes as one 8-byte store.
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+constexpr int kWavesQ = 4;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+__global__ void __launch_bounds__(64 * kWavesQ) quantize_kernel(const __bf16* __restrict__ x, int8_t* __restrict__ codes,
+                                                               float* __restrict__ scales, int T, int d) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kWavesQ + (threadIdx.x >> 6);
+  if (row >= T) return;
+  const uint4* src = reinterpret_cast<const uint4*>(x + (size_t)row * d);
+  const int n8 = d / 8;  // 16-byte chunks per row (d % 64 == 0)
+  float m = 0.f;
+  for (int c = lane; c < n8; c += 64) {
+    const uint4 v = src[c];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) m = fmaxf(m, fmaxf(fabsf(bf16_lo(w[i])), fabsf(bf16_hi(w[i]))));
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  const float scale = m / 127.0f;
+  if (lane == 0) scales[row] = scale;
+  uint2* dst = reinterpret_cast<uint2*>(codes + (size_t)row * d);
+  for (int c = lane; c < n8; c += 64) {
+    const uint4 v = src[c];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t out[2] = {0u, 0u};
+    if (scale > 0.f) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float f[2] = {bf16_lo(w[i]), bf16_hi(w[i])};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float q = fminf(fmaxf(rintf(f[h] / scale), -127.f), 127.f);
+          const uint32_t b = (uint32_t)((int)q) & 0xFFu;
+          out[i / 2] |= b << (8 * (2 * (i % 2) + h));
+        }
+      }
+    }
+    dst[c] = make_uint2(out[0], out[1]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const void* x, int8_t* codes, float* scales, int T, int d, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  if (d <= 0 || d % 64 != 0) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)((T + kWavesQ - 1) / kWavesQ);
+  hipLaunchKernelGGL(quantize_kernel, dim3(grid), dim3(64 * kWavesQ), 0, s, static_cast<const __bf16*>(x), codes,
+                     scales, T, d);
+  return hipGetLastError();
+}
+
+}  // namespace moe

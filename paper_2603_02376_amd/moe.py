@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_PKG, "libmoe.so")
 MOE_F32, MOE_BF16 = 0, 1
 MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_LAYOUT_ROWMAJOR, MOE_LAYOUT_PACKED = 0, 1
+MOE_QUANT_NONE, MOE_QUANT_INT8 = 0, 1
 STATUS = {0: "MOE_OK", -1: "MOE_ERR_INVALID_ARG", -2: "MOE_ERR_UNSUPPORTED",
           -3: "MOE_ERR_WORKSPACE", -4: "MOE_ERR_HIP"}
 
@@ -37,7 +38,7 @@ class moe_config_t(ctypes.Structure):
                 ("n_groups", ctypes.c_int32), ("topk_groups", ctypes.c_int32), ("I", ctypes.c_int32),
                 ("n_shared", ctypes.c_int32), ("I_shared", ctypes.c_int32), ("score", ctypes.c_int32),
                 ("renorm", ctypes.c_int32), ("route_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
-                ("weight_layout", ctypes.c_int32)]
+                ("weight_layout", ctypes.c_int32), ("token_quant", ctypes.c_int32)]
 
 
 class moe_layer_debug_t(ctypes.Structure):
@@ -54,6 +55,8 @@ _SIGS = {
     "moe_dispatch": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_expert_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_shared_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "moe_quantize": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP]),
+    "moe_expert_ffn_q8": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_combine": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
     "moe_layer": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ,
                                  _VP, _VP, ctypes.POINTER(moe_layer_debug_t)]),
@@ -106,6 +109,7 @@ class MoeConfig:
     scale: float = 1.0
     dtype: str = "bf16"        # "bf16" | "f32"
     weight_layout: str = "rowmajor"  # "rowmajor" | "packed" (expert weights, see moe_pack_weights)
+    token_quant: str = "none"        # "none" | "int8" (tokens the routed experts receive)
 
     @property
     def torch_dtype(self):
@@ -116,7 +120,8 @@ class MoeConfig:
                             self.I_shared, MOE_SCORE_SIGMOID if self.score == "sigmoid" else MOE_SCORE_SOFTMAX,
                             int(bool(self.renorm)), float(self.scale),
                             MOE_BF16 if self.dtype == "bf16" else MOE_F32,
-                            MOE_LAYOUT_PACKED if self.weight_layout == "packed" else MOE_LAYOUT_ROWMAJOR)
+                            MOE_LAYOUT_PACKED if self.weight_layout == "packed" else MOE_LAYOUT_ROWMAJOR,
+                            MOE_QUANT_INT8 if self.token_quant == "int8" else MOE_QUANT_NONE)
 
     @property
     def packed(self) -> bool:
@@ -206,6 +211,30 @@ def moe_expert_ffn(cfg: MoeConfig, T, x, sorted_token, offsets, w_gate, w_up, w_
                                 _ptr(w_gate, "w_gate", dt, gsz), _ptr(w_up, "w_up", dt, wsz),
                                 _ptr(w_down, "w_down", dt, wsz), _ptr(y_perm, "y_perm", dt, n * cfg.d),
                                 _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_quantize(cfg: MoeConfig, T, x, codes, scales, stream=None):
+    """Per-token int8 quantization: codes int8 [T, d], scales fp32 [T]."""
+    c = cfg.c()
+    _check(lib().moe_quantize(ctypes.byref(c), T, _ptr(x, "x", cfg.torch_dtype, T * cfg.d),
+                              _ptr(codes, "codes", torch.int8, T * cfg.d), _ptr(scales, "scales", torch.float32, T),
+                              _stream(stream)))
+
+
+def moe_expert_ffn_q8(cfg: MoeConfig, T, codes, scales, sorted_token, offsets, w_gate_up, w_down, y_perm, ws,
+                      stream=None):
+    """Expert FFN on int8 tokens (packed weights from :func:`pack_weights`)."""
+    c = cfg.c()
+    n = T * cfg.k
+    wsz = cfg.E * cfg.I * cfg.d
+    _check(lib().moe_expert_ffn_q8(ctypes.byref(c), T, _ptr(codes, "codes", torch.int8, T * cfg.d),
+                                   _ptr(scales, "scales", torch.float32, T),
+                                   _ptr(sorted_token, "sorted_token", torch.int32, n),
+                                   _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                                   _ptr(w_gate_up, "w_gate_up", torch.bfloat16, 2 * wsz),
+                                   _ptr(w_down, "w_down", torch.bfloat16, wsz),
+                                   _ptr(y_perm, "y_perm", torch.bfloat16, n * cfg.d),
+                                   _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def moe_shared_ffn(cfg: MoeConfig, T, x, ws_gate, ws_up, ws_down, out, ws, stream=None):

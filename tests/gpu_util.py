@@ -32,7 +32,8 @@ def moe_cfg(p: dict) -> moe.MoeConfig:
     return moe.MoeConfig(d=p["d"], E=p["E"], k=p["k"], I=p["I"], n_groups=p.get("n_groups", 1),
                          topk_groups=p.get("topk_groups", 1), n_shared=p.get("n_shared", 0),
                          I_shared=p.get("I_shared", 0), score=p["score"], renorm=p.get("renorm", True),
-                         scale=p.get("scale", 1.0), dtype=p["dtype"], weight_layout=p.get("weight_layout", "rowmajor"))
+                         scale=p.get("scale", 1.0), dtype=p["dtype"], weight_layout=p.get("weight_layout", "rowmajor"),
+                         token_quant=p.get("token_quant", "none"))
 
 
 def oracle_cfg(p: dict) -> dict:
