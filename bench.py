@@ -78,7 +78,7 @@ def measured_traffic(workload: str, layout: str):
 
 
 def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens: int = 64,
-                 ffn_only: bool = False, layout: str = "packed", multilayer: tuple = ()):
+                 ffn_only: bool = False, layout: str = "packed", multilayer: tuple = (), int8: bool = False):
     import numpy as np
     import torch
 
@@ -178,8 +178,46 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
     torch.cuda.synchronize()
     ffn_ms = f0.elapsed_time(f1) / steps
 
+    # int8 tokens (the pipeline's quantize-before-dispatch): the quantize
+    # kernel, the expert FFN on the codes and the layer with int8 tokens
+    q8 = None
+    if int8 and cfg.packed and not ffn_only:
+        import dataclasses
+
+        codes = torch.empty((T, p["d"]), dtype=torch.int8, device="cuda")
+        scales = torch.empty(T, dtype=torch.float32, device="cuda")
+        cfg8 = dataclasses.replace(cfg, token_quant="int8")
+        ws8 = moe.alloc_workspace(cfg8, T)
+
+        def timed(fn, n):
+            for _ in range(max(2, warmup)):
+                fn()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s_main)
+            for _ in range(n):
+                fn()
+            b.record(s_main)
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / n
+
+        q_ms = timed(lambda: moe.moe_quantize(cfg, T, t["x"], codes, scales, stream=s_main), steps)
+        f8_ms = timed(lambda: moe.moe_expert_ffn_q8(cfg, T, codes, scales, dbg["sorted_token"], dbg["offsets"],
+                                                     w_ffn[0], w_ffn[2], y, ws, stream=s_main), steps)
+        l8_ms = timed(lambda: moe.moe_layer(cfg8, T, t["x"], t["w_router"], t["bias"], *w_ffn, *w_sh, out, ws8,
+                                            s_main=s_main, s_aux=s_aux), steps)
+        # token bytes the GEMM1 operand loads gather (every column tile reads its rows again)
+        nt1 = p["I"] // 128
+        rows = T * p["k"]
+        q8 = dict(quantize_ms=round(q_ms, 4), expert_ffn_ms=round(f8_ms, 4),
+                  expert_ffn_speedup=round(ffn_ms / f8_ms, 4), layer_ms=round(l8_ms, 4),
+                  tokens_per_s=round(T / (l8_ms / 1e3), 1),
+                  gathered_token_bytes_gemm1={"bf16": nt1 * rows * p["d"] * 2, "int8": nt1 * rows * p["d"]},
+                  note="layer with int8 tokens runs the shared expert outside the routed GEMMs")
+        del codes, scales, ws8
+
     res = dict(
-        name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms,
+        name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms, int8_tokens=q8,
         counts_max_over_mean=float(counts.max() / counts.mean()), empty_experts=int((counts == 0).sum()),
         layer_hbm_frac=alg["layer_bytes"] / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
         layer_mfma_frac=alg["layer_flops"] / (ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12),
@@ -278,7 +316,8 @@ def main():
         log(f"[bench] copy calibration: 3 x {n} B, {2 * 3 * n / (c0.elapsed_time(c1) / 1e3) / 1e9:.1f} GB/s")
         del src, dst
     main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_tokens,
-                            args.ffn_only, args.layout, multilayer=() if args.no_extra else (1, 4, 16))
+                            args.ffn_only, args.layout, multilayer=() if args.no_extra else (1, 4, 16),
+                            int8=not args.no_extra)
     if args.ffn_only:
         print(json.dumps(dict(workload=args.workload, expert_ffn_ms=main_res["ffn_ms"],
                               expert_ffn_gbs=main_res["ffn_gbs"], expert_ffn_tflops=main_res["ffn_tflops"])))
@@ -288,7 +327,7 @@ def main():
         for name in ("dsv3_skew", "dsv3_decode", "mixtral"):
             if name == args.workload:
                 continue
-            r = run_workload(name, args.steps, args.warmup, False, layout=args.layout)
+            r = run_workload(name, args.steps, args.warmup, False, layout=args.layout, int8=name == "dsv3_decode")
             extra[name] = dict(tokens_per_s=round(r["tokens_per_s"], 1), ms_per_step=round(r["ms"], 4),
                                layer_hbm_frac=round(r["layer_hbm_frac"], 4),
                                layer_mfma_frac=round(r["layer_mfma_frac"], 4),
@@ -297,6 +336,8 @@ def main():
                                expert_ffn_roofline_frac=round(r["ffn_roof_frac"], 4),
                                touched_experts=r["alg"]["touched_experts"],
                                max_over_mean_load=round(r["counts_max_over_mean"], 3), empty_experts=r["empty_experts"])
+            if r["int8_tokens"]:
+                extra[name]["int8_tokens"] = r["int8_tokens"]
 
     r = main_res
     p = r["p"]
@@ -339,6 +380,8 @@ def main():
     }
     if "cpu" in r:
         out["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r["cpu"].items()}
+    if r["int8_tokens"]:
+        out["int8_tokens"] = r["int8_tokens"]
     if r["multilayer_ms_per_layer"]:
         out["multilayer"] = {"ms_per_layer": {str(L): round(v, 4) for L, v in r["multilayer_ms_per_layer"].items()},
                              "note": "L layer calls back to back on the same input and weights, each into its own output"}
