@@ -1,12 +1,12 @@
 // Combine: the single-GPU form of the paper's combine all-to-all (App. F,
 // second exchange), out[t] = sum_j w[t][j] * y_perm[inv_perm[t*k+j]] (+ shared[t]).
 //
-// Atomic-free: one workgroup owns one output row and gathers its k expert
-// rows through the inverse permutation, so the sum order (j ascending, then
-// the shared expert) is fixed and the result is bit-reproducible. The kernel
-// is HBM-bound (k+1 rows read, one written per token); every thread moves 8
-// elements per access (16 bytes for bf16) and keeps the k row indices and
-// weights in registers.
+// Atomic-free: each output element is produced by one thread, which gathers
+// the token's k expert rows through the inverse permutation, so the sum
+// order (j ascending, then the shared expert) is fixed and the result is
+// bit-reproducible. The kernel is HBM-bound (k+1 rows read, one written per
+// token); every thread moves 8 elements per access (16 bytes for bf16) and
+// keeps the k row indices and weights in registers.
 #include "moe_internal.h"
 
 namespace moe {
@@ -55,9 +55,15 @@ __device__ __forceinline__ void store8(float* p, const Vec8& x) {
   *reinterpret_cast<f32x4*>(p + 4) = b;
 }
 
+// One workgroup per (token, chunk of kThreads * 8 elements): every thread
+// produces 8 output elements. Many small workgroups (T * d / 1024 of them)
+// keep the tail of the launch short; the k row indices and weights of the
+// token are loaded by every workgroup of that token (uniform loads).
 template <typename T>
 __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
-  const int t = blockIdx.x;
+  const int nch = (p.d + kThreads * 8 - 1) / (kThreads * 8);  // chunks per row
+  const int t = blockIdx.x / nch;                               // token-major: a token's chunks are adjacent
+  const int c = ((blockIdx.x % nch) * kThreads + threadIdx.x) * 8;
   const int k = p.k;
   const size_t d = (size_t)p.d;
   const T* Y = static_cast<const T*>(p.y_perm);
@@ -72,35 +78,38 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
       w[j] = p.topk_w[(size_t)t * k + j];
     }
   }
-  for (int c = threadIdx.x * 8; c < p.d; c += kThreads * 8) {
-    Vec8 acc;
+  if (c >= p.d) return;
+  Vec8 acc;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc.v[i] = 0.f;
+  for (int i = 0; i < 8; ++i) acc.v[i] = 0.f;
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-      if (j < k) {
-        const Vec8 y = load8(Y + (size_t)rows[j] * d + c);
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j < k) {
+      const Vec8 y = load8(Y + (size_t)rows[j] * d + c);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc.v[i] = fmaf(w[j], y.v[i], acc.v[i]);
-      }
+      for (int i = 0; i < 8; ++i) acc.v[i] = fmaf(w[j], y.v[i], acc.v[i]);
     }
-    if (S) {
-      const Vec8 s = load8(S + (size_t)t * d + c);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc.v[i] += s.v[i];
-    }
-    store8(O + (size_t)t * d + c, acc);
   }
+  if (S) {
+    const Vec8 s = load8(S + (size_t)t * d + c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc.v[i] += s.v[i];
+  }
+  store8(O + (size_t)t * d + c, acc);
 }
 
 }  // namespace
 
 hipError_t launch_combine(const CombineParams& p, bool bf16, hipStream_t s) {
   if (p.T <= 0) return hipSuccess;
+  if (p.k > kMaxK) return hipErrorInvalidValue;
+  const long long blocks = (long long)((p.d + kThreads * 8 - 1) / (kThreads * 8)) * p.T;
+  if (blocks > 0x7FFFFFFFll) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks);
   if (bf16)
-    hipLaunchKernelGGL(combine_kernel<__bf16>, dim3(p.T), dim3(kThreads), 0, s, p);
+    hipLaunchKernelGGL(combine_kernel<__bf16>, grid, dim3(kThreads), 0, s, p);
   else
-    hipLaunchKernelGGL(combine_kernel<float>, dim3(p.T), dim3(kThreads), 0, s, p);
+    hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
