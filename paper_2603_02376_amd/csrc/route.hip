@@ -69,18 +69,39 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
   // ---- scores and keys ---------------------------------------------------
   double key[EPL], score[EPL];
   float u[EPL];
+  // Logits: the K-split partials summed in ascending split order. Each
+  // round issues the loads of up to 8 splits for all of the lane's experts
+  // before adding them, so the loads overlap instead of waiting one by one.
+  {
+    constexpr int R = 8;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = lane * EPL + i;
+      u[i] = (active && e < E) ? p.logits_in[(size_t)t * E + e] : 0.f;
+    }
+    for (int sp0 = 1; sp0 < p.nsplit; sp0 += R) {
+      float part[R][EPL];
+#pragma unroll
+      for (int q = 0; q < R; ++q)
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) {
+          const int e = lane * EPL + i;
+          part[q][i] = (active && e < E && sp0 + q < p.nsplit)
+                           ? p.logits_in[(size_t)(sp0 + q) * p.split_stride + (size_t)t * E + e]
+                           : 0.f;
+        }
+#pragma unroll
+      for (int q = 0; q < R; ++q)
+#pragma unroll
+        for (int i = 0; i < EPL; ++i)
+          if (sp0 + q < p.nsplit) u[i] += part[q][i];
+    }
+  }
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane * EPL + i;
     const bool ok = active && e < E;
-    float v = 0.f;
-    if (ok) {
-      const float* src = p.logits_in + (size_t)t * E + e;
-      v = src[0];
-      for (int sp = 1; sp < p.nsplit; ++sp) v += src[(size_t)sp * p.split_stride];
-      if (p.logits_out) p.logits_out[(size_t)t * E + e] = v;
-    }
-    u[i] = v;
+    if (ok && p.logits_out) p.logits_out[(size_t)t * E + e] = u[i];
     if (!ok) {
       key[i] = NEG;
       score[i] = 0.0;
