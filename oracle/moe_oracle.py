@@ -35,8 +35,10 @@ brute-force enumeration on tiny inputs, special cases that reduce to a dense
 SwiGLU or a dense softmax mixture, and invariants; the token quantization by
 hand-derived examples with exact power-of-two scales, its error bound and the
 quantized layer's reduction to the plain one on exactly representable
-tokens). The layer as a whole has no value printed in the paper; it is pinned
-only through those pieces.
+tokens; the expert-parallel receive plan by hand-derived examples and
+invariants, its FFN by its reduction to the single-GPU expert FFN). The layer
+as a whole has no value printed in the paper; it is pinned only through those
+pieces.
 """
 
 from __future__ import annotations
@@ -56,6 +58,8 @@ __all__ = [
     "layer_rows",
     "quantize_tokens",
     "dequantize_tokens",
+    "ep_receive_plan",
+    "ep_receive_ffn",
 ]
 
 
@@ -313,6 +317,64 @@ def quantize_tokens(x):
 def dequantize_tokens(codes, scales) -> np.ndarray:
     """``codes[t, c] * scales[t]`` in fp64 (the tokens GEMM1 sees)."""
     return np.asarray(codes, dtype=np.float64) * np.asarray(scales, dtype=np.float64)[:, None]
+
+
+# ---------------------------------------------------------------------------
+# expert parallelism, receive side (App. M: each GPU owns some experts; the
+# dispatch exchange brings it the rows of its own tokens and of its peer's
+# tokens routed to those experts; §4.3: the self rows are ready at once, the
+# remote rows once the exchange has delivered them)
+# ---------------------------------------------------------------------------
+
+def ep_receive_plan(self_offsets, self_sorted_token, peer_offsets, peer_sorted_token, e_first: int, e_count: int):
+    """Rows a GPU owning global experts [e_first, e_first + e_count) receives.
+
+    Inputs are the two ranks' dispatches over the global experts (``offsets``
+    and ``sorted_token`` as returned by :func:`dispatch`). Local expert ``e``
+    (global ``e_first + e``) gets this GPU's rows of that expert, then the
+    peer's, each in dispatch order. Returns ``row_token`` (token of each row
+    in its own rank's input), ``offsets [e_count+1]`` and ``self_end
+    [e_count]`` (rows ``[offsets[e], self_end[e])`` are this GPU's tokens),
+    all int32.
+    """
+    so = np.asarray(self_offsets, dtype=np.int64)
+    po = np.asarray(peer_offsets, dtype=np.int64)
+    st = np.asarray(self_sorted_token, dtype=np.int64)
+    pt = np.asarray(peer_sorted_token, dtype=np.int64)
+    rows = []
+    offsets = [0]
+    self_end = []
+    for e in range(e_count):
+        g = e_first + e
+        mine = list(st[so[g]:so[g + 1]])
+        theirs = list(pt[po[g]:po[g + 1]])
+        rows += mine
+        self_end.append(offsets[-1] + len(mine))
+        rows += theirs
+        offsets.append(offsets[-1] + len(mine) + len(theirs))
+    return (np.asarray(rows, dtype=np.int32), np.asarray(offsets, dtype=np.int32),
+            np.asarray(self_end, dtype=np.int32))
+
+
+def ep_receive_ffn(x_self, x_peer, row_token, offsets, self_end, w_gate, w_up, w_down, rows=None) -> np.ndarray:
+    """Expert FFN of received rows, in fp64: row ``r`` of local expert ``e`` is
+    token ``row_token[r]`` of ``x_self`` (below ``self_end[e]``) or of
+    ``x_peer``; the weights are indexable by local expert. ``rows``: compute
+    only these rows (all if None); returns ``[len(rows), d]``."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    self_end = np.asarray(self_end, dtype=np.int64)
+    row_token = np.asarray(row_token, dtype=np.int64)
+    n = int(offsets[-1])
+    rows = np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64)
+    Xs, Xp = to_f64(x_self), to_f64(x_peer)
+    out = np.zeros((rows.size, Xs.shape[1]))
+    expert = np.searchsorted(offsets, rows, side="right") - 1
+    for e in np.unique(expert):
+        sel = np.nonzero(expert == e)[0]
+        r = rows[sel]
+        src = np.where((r < self_end[e])[:, None], Xs[row_token[r]], Xp[row_token[r]])
+        out[sel] = swiglu_ffn(src, w_gate[e], w_up[e], w_down[e])
+    return out
 
 
 # ---------------------------------------------------------------------------

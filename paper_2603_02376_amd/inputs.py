@@ -20,13 +20,23 @@ expert weights N(0, 1/sqrt(fan_in)), seed 0):
                   the paper's 2:1-5:1 routing imbalance, §4 Workloads).
 * ``dsv3_decode`` as ``dsv3`` with T=128.
 
+Expert parallelism over two GPUs (the paper's MoE evaluation, §4 and App. M:
+two ranks, 4096 tokens each, routing imbalance ratios 2:1 to 5:1): the 256
+experts split into two halves, this GPU owning the first. :func:`ep_topk`
+draws each rank's top-k directly (the routing is an input here): each of a
+token's k experts lies in the first half with probability r/(r+1), so that
+half receives r/(r+1) of all assignments; the experts are drawn uniformly
+without replacement within each half. :func:`ep_peer_tokens` draws the peer
+rank's tokens.
+
 Random streams: host tensors use ``numpy.random.Generator(PCG64(SeedSequence(
 [seed, tensor_id, expert])))``, draws in float32; the multi-GB expert
 weights are drawn on the target device with ``torch.randn`` from a generator
 seeded with ``seed * 1000 + tensor_id`` (deterministic per device type).
 bf16 tensors are the round-to-nearest-even cast of those float32 draws.
 Tensor ids: x 0, router 1, expert gate 3, up 4, down 5, shared gate 6, up 7,
-down 8, Zipf expert order 9.
+down 8, Zipf expert order 9, expert-parallel top-k of this rank 10 and of
+the peer 11, peer tokens 12.
 """
 from __future__ import annotations
 
@@ -57,7 +67,9 @@ ZIPF_ALPHA = 1.2
 ZIPF_BETA = 0.050971
 ZIPF_TARGET_MAX_OVER_MEAN = 10.0
 
-TENSOR_IDS = dict(x=0, w_router=1, bias=2, w_gate=3, w_up=4, w_down=5, ws_gate=6, ws_up=7, ws_down=8, zipf_order=9)
+TENSOR_IDS = dict(x=0, w_router=1, bias=2, w_gate=3, w_up=4, w_down=5, ws_gate=6, ws_up=7, ws_down=8, zipf_order=9,
+                  ep_topk_self=10, ep_topk_peer=11, x_peer=12)
+EP_RATIOS = (2, 3, 4, 5)  # routing imbalance ratios r:1 of the paper's MoE evaluation
 
 
 def preset(name: str, **overrides) -> dict:
@@ -80,6 +92,30 @@ def zipf_bias(E: int, seed: int = 0, alpha: float = ZIPF_ALPHA, beta: float | No
     p = rank.astype(np.float64) ** (-alpha)
     p /= p.sum()
     return (beta * np.log(E * p)).astype(np.float32)
+
+
+def ep_topk(T: int, E: int, k: int, ratio: float, side: str = "self", seed: int = 0) -> np.ndarray:
+    """int32 [T, k]: every token's k distinct experts, each in [0, E/2) with
+    probability ratio/(ratio+1) (binomial count per token, capped by the half's
+    size), uniform without replacement within each half; slots in a random
+    order. side: "self" or "peer" (independent streams)."""
+    if E % 2 or k > E // 2:
+        raise ValueError("need an even E and k <= E/2")
+    rng = host_rng(seed, "ep_topk_self" if side == "self" else "ep_topk_peer", int(round(ratio * 1000)))
+    half = E // 2
+    p = ratio / (ratio + 1.0)
+    n0 = np.minimum(rng.binomial(k, p, size=T), half)
+    out = np.empty((T, k), dtype=np.int32)
+    for t in range(T):
+        a = rng.choice(half, size=int(n0[t]), replace=False)
+        b = half + rng.choice(half, size=k - int(n0[t]), replace=False)
+        out[t] = rng.permutation(np.concatenate([a, b]))
+    return out
+
+
+def ep_peer_tokens(T: int, d: int, seed: int = 0) -> np.ndarray:
+    """float32 [T, d] N(0, 1): the peer rank's tokens."""
+    return host_rng(seed, "x_peer").standard_normal((T, d), dtype=np.float32)
 
 
 def host_activations(cfg: dict, seed: int = 0):

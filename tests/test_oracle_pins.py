@@ -533,3 +533,94 @@ def test_layer_rows_quantized_agrees_with_full_layer():
     rows = np.array([0, 5, 23])
     part = O.layer_rows(x, rows, full["topk_idx"][rows], full["topk_w"][rows], wg, wu, wd, sg, su, sd, quant="int8")
     np.testing.assert_allclose(part, full["out"][rows], rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# expert parallelism, receive side
+# ---------------------------------------------------------------------------
+
+def test_ep_receive_plan_worked_examples():
+    ex = json.load(open(os.path.join(GOLDEN, "ep_plan_examples.json")))
+    s = O.dispatch(np.asarray(ex["self_topk"]), ex["E"])
+    p = O.dispatch(np.asarray(ex["peer_topk"]), ex["E"])
+    for name in ("P1", "P2"):
+        e = ex[name]
+        rt, off, se = O.ep_receive_plan(s[1], s[2], p[1], p[2], e["e_first"], e["e_count"])
+        assert rt.tolist() == e["row_token"], name
+        assert off.tolist() == e["offsets"], name
+        assert se.tolist() == e["self_end"], name
+
+
+def _ep_plan_brute(self_topk, peer_topk, e_first, e_count):
+    """The receive plan by enumeration: for each local expert, scan the
+    tokens of each rank in order and keep those that chose it."""
+    rows, offsets, self_end = [], [0], []
+    for e in range(e_first, e_first + e_count):
+        mine = [t for t, r in enumerate(self_topk) if e in list(r)]
+        theirs = [t for t, r in enumerate(peer_topk) if e in list(r)]
+        rows += mine
+        self_end.append(offsets[-1] + len(mine))
+        rows += theirs
+        offsets.append(offsets[-1] + len(mine) + len(theirs))
+    return rows, offsets, self_end
+
+
+@pytest.mark.parametrize("ratio", [1.0, 3.0, 5.0])
+def test_ep_receive_plan_matches_enumeration_and_invariants(ratio):
+    from paper_2603_02376_amd import inputs
+    T, E, k = 40, 16, 3
+    st = inputs.ep_topk(T, E, k, ratio, "self", seed=1)
+    pt = inputs.ep_topk(T, E, k, ratio, "peer", seed=1)
+    s, p = O.dispatch(st, E), O.dispatch(pt, E)
+    for e_first, e_count in ((0, E // 2), (E // 2, E // 2), (3, 5)):
+        rt, off, se = O.ep_receive_plan(s[1], s[2], p[1], p[2], e_first, e_count)
+        rows, offsets, self_end = _ep_plan_brute(st, pt, e_first, e_count)
+        assert rt.tolist() == rows and off.tolist() == offsets and se.tolist() == self_end
+        # every local assignment of either rank appears exactly once
+        local = lambda tk: sorted((t, int(e)) for t, r in enumerate(tk) for e in r if e_first <= e < e_first + e_count)
+        got_self = sorted((int(rt[r]), e_first + e) for e in range(e_count) for r in range(off[e], se[e]))
+        got_peer = sorted((int(rt[r]), e_first + e) for e in range(e_count) for r in range(se[e], off[e + 1]))
+        assert got_self == local(st) and got_peer == local(pt)
+
+
+def test_ep_topk_ratio_and_distinct_experts():
+    from paper_2603_02376_amd import inputs
+    T, E, k = 4096, 256, 8
+    for r in inputs.EP_RATIOS:
+        tk = inputs.ep_topk(T, E, k, r, "self")
+        assert tk.dtype == np.int32 and tk.shape == (T, k)
+        assert all(len(set(row)) == k for row in tk)
+        assert tk.min() >= 0 and tk.max() < E
+        frac = (tk < E // 2).mean()
+        # binomial mean r/(r+1); 32768 draws: standard error < 0.003
+        assert abs(frac - r / (r + 1)) < 0.015, (r, frac)
+    assert not np.array_equal(inputs.ep_topk(64, E, k, 3, "self"), inputs.ep_topk(64, E, k, 3, "peer"))
+
+
+def test_ep_receive_ffn_reduces_to_each_ranks_expert_ffn():
+    # every received row is the single-GPU expert FFN of its token, whichever
+    # rank it came from
+    from paper_2603_02376_amd import inputs
+    rng = np.random.default_rng(5)
+    T, E, k, d, I = 12, 8, 2, 16, 8
+    xs, xp = rng.standard_normal((T, d)), rng.standard_normal((T, d))
+    wg, wu = rng.standard_normal((E, I, d)) * 0.3, rng.standard_normal((E, I, d)) * 0.3
+    wd = rng.standard_normal((E, d, I)) * 0.3
+    st, pt = inputs.ep_topk(T, E, k, 2.0, "self", 2), inputs.ep_topk(T, E, k, 2.0, "peer", 2)
+    s, p = O.dispatch(st, E), O.dispatch(pt, E)
+    ys = O.expert_ffn(xs, s[2], s[1], wg, wu, wd)
+    yp = O.expert_ffn(xp, p[2], p[1], wg, wu, wd)
+    e0, ne = E // 2, E // 2
+    rt, off, se = O.ep_receive_plan(s[1], s[2], p[1], p[2], e0, ne)
+    y = O.ep_receive_ffn(xs, xp, rt, off, se, wg[e0:], wu[e0:], wd[e0:])
+    # (fp64 matrix products of differently batched rows may differ in the last bits)
+    for e in range(ne):
+        g = e0 + e
+        np.testing.assert_allclose(y[off[e]:se[e]], ys[s[1][g]:s[1][g + 1]], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(y[se[e]:off[e + 1]], yp[p[1][g]:p[1][g + 1]], rtol=1e-12, atol=1e-12)
+    sub = [0, int(off[-1]) - 1, int(se[1])]
+    np.testing.assert_allclose(O.ep_receive_ffn(xs, xp, rt, off, se, wg[e0:], wu[e0:], wd[e0:], rows=sub), y[sub],
+                               rtol=1e-12, atol=1e-12)
+    # a planted swap of the row sources (self rows read from the peer) is caught
+    bad = O.ep_receive_ffn(xp, xs, rt, off, se, wg[e0:], wu[e0:], wd[e0:])
+    assert not np.allclose(bad, y, rtol=1e-6)
