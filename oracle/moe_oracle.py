@@ -372,7 +372,10 @@ def ep_receive_ffn(x_self, x_peer, row_token, offsets, self_end, w_gate, w_up, w
     for e in np.unique(expert):
         sel = np.nonzero(expert == e)[0]
         r = rows[sel]
-        src = np.where((r < self_end[e])[:, None], Xs[row_token[r]], Xp[row_token[r]])
+        mine = r < self_end[e]
+        src = np.empty((r.size, Xs.shape[1]))
+        src[mine] = Xs[row_token[r[mine]]]
+        src[~mine] = Xp[row_token[r[~mine]]]
         out[sel] = swiglu_ffn(src, w_gate[e], w_up[e], w_down[e])
     return out
 

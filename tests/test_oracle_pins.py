@@ -602,11 +602,11 @@ def test_ep_receive_ffn_reduces_to_each_ranks_expert_ffn():
     # rank it came from
     from paper_2603_02376_amd import inputs
     rng = np.random.default_rng(5)
-    T, E, k, d, I = 12, 8, 2, 16, 8
-    xs, xp = rng.standard_normal((T, d)), rng.standard_normal((T, d))
+    T, Tp, E, k, d, I = 12, 5, 8, 2, 16, 8   # the peer has fewer tokens than this GPU
+    xs, xp = rng.standard_normal((T, d)), rng.standard_normal((Tp, d))
     wg, wu = rng.standard_normal((E, I, d)) * 0.3, rng.standard_normal((E, I, d)) * 0.3
     wd = rng.standard_normal((E, d, I)) * 0.3
-    st, pt = inputs.ep_topk(T, E, k, 2.0, "self", 2), inputs.ep_topk(T, E, k, 2.0, "peer", 2)
+    st, pt = inputs.ep_topk(T, E, k, 2.0, "self", 2), inputs.ep_topk(Tp, E, k, 2.0, "peer", 2)
     s, p = O.dispatch(st, E), O.dispatch(pt, E)
     ys = O.expert_ffn(xs, s[2], s[1], wg, wu, wd)
     yp = O.expert_ffn(xp, p[2], p[1], wg, wu, wd)
@@ -621,6 +621,8 @@ def test_ep_receive_ffn_reduces_to_each_ranks_expert_ffn():
     sub = [0, int(off[-1]) - 1, int(se[1])]
     np.testing.assert_allclose(O.ep_receive_ffn(xs, xp, rt, off, se, wg[e0:], wu[e0:], wd[e0:], rows=sub), y[sub],
                                rtol=1e-12, atol=1e-12)
-    # a planted swap of the row sources (self rows read from the peer) is caught
-    bad = O.ep_receive_ffn(xp, xs, rt, off, se, wg[e0:], wu[e0:], wd[e0:])
+    # a planted swap of the row sources (self rows read from the peer's tokens) is caught
+    xs2 = xs.copy()
+    xs2[:Tp] = xp
+    bad = O.ep_receive_ffn(xs2, xp, rt, off, se, wg[e0:], wu[e0:], wd[e0:])
     assert not np.allclose(bad, y, rtol=1e-6)
