@@ -13,8 +13,11 @@ the plain [E][I][d] weights instead. Prints ONE JSON line: tokens/s of the
 layer, the roofline of the dominant kernel pair (the grouped expert FFN,
 timed with HIP events on its own stream), the CPU oracle timed on a bounded
 sample of the same workload as a baseline, the per-layer time of 1, 4 and 16
-layer calls run back to back, and side measurements of the skewed-routing,
-decode-sized and Mixtral-shaped workloads (--no-extra skips these).
+layer calls run back to back, the receive side of two-GPU expert parallelism
+under the three schedules of moe_ep_expert_ffn for imbalance ratios 2:1 to
+5:1 (the exchange emulated by a copy with a fixed workgroup budget), and side
+measurements of the skewed-routing, decode-sized and Mixtral-shaped
+workloads (--no-extra skips these).
 """
 from __future__ import annotations
 
@@ -77,8 +80,106 @@ def measured_traffic(workload: str, layout: str):
     return rec.get("bytes_per_call")
 
 
+EP_LINK_WORKGROUPS = 16  # workgroups of the emulated exchange (~77 GB/s measured: about one xGMI link, one way)
+EP_CHUNKS = (4, 8, 16)
+
+
+def ep_split(p: dict, x, gate_up, down, steps: int, warmup: int) -> dict:
+    """Receive side of two-GPU expert parallelism (App. M; §4.3, Table 5) on
+    one GPU: this GPU owns experts [0, E/2) of the workload, each rank has T
+    tokens, and a fraction r/(r+1) of all assignments goes to this GPU's
+    experts (r = 2..5). The remote rows arrive through a copy limited to
+    EP_LINK_WORKGROUPS workgroups on its own stream (the emulated link); the
+    expert GEMMs keep the other compute units while rows still arrive.
+    Times moe_ep_expert_ffn under each schedule, plus the link and the FFN
+    alone, and the FFN of the self rows and of the remote rows as two calls
+    (the split's two passes over every expert's weights)."""
+    import torch
+
+    from paper_2603_02376_amd import inputs, moe
+
+    T, d, Eg, k, I = p["T"], p["d"], p["E"], p["k"], p["I"]
+    E = Eg // 2
+    cfg = moe.MoeConfig(d=d, E=E, k=k, I=I, dtype="bf16", weight_layout="packed")
+    gcfg = moe.MoeConfig(d=d, E=Eg, k=k, I=I, dtype="bf16")
+    xp = torch.from_numpy(inputs.ep_peer_tokens(T, d)).to(device="cuda", dtype=torch.bfloat16)
+    s_c = torch.cuda.current_stream()
+    link = torch.cuda.Stream()
+    gemm_wg = torch.cuda.get_device_properties(0).multi_processor_count - EP_LINK_WORKGROUPS // 2
+    gemm_wg -= gemm_wg % 8
+    n_steps = max(3, min(steps, 10))
+
+    def timed(fn):
+        for _ in range(max(2, warmup // 2)):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s_c)
+        for _ in range(n_steps):
+            fn()
+        b.record(s_c)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n_steps
+
+    def dispatch(tk):
+        ws = moe.alloc_workspace(gcfg, T)
+        z = lambda m: torch.empty(m, dtype=torch.int32, device="cuda")
+        c, o, st, sa, inv = z(Eg), z(Eg + 1), z(T * k), z(T * k), z(T * k)
+        moe.moe_dispatch(gcfg, T, torch.from_numpy(tk).cuda(), c, o, st, sa, inv, ws)
+        return o, st
+
+    ratios = []
+    link_gbs = []
+    for r in inputs.EP_RATIOS:
+        so, ss = dispatch(inputs.ep_topk(T, Eg, k, r, "self"))
+        po, ps = dispatch(inputs.ep_topk(T, Eg, k, r, "peer"))
+        n_self, n = int(so[E].item()), int(so[E].item()) + int(po[E].item())
+        rt = torch.empty(n, dtype=torch.int32, device="cuda")
+        off = torch.empty(E + 1, dtype=torch.int32, device="cuda")
+        se = torch.empty(E, dtype=torch.int32, device="cuda")
+        moe.moe_ep_plan(cfg, 0, so, ss, T * k, po, ps, T * k, rt, n, off, se)
+        recv = torch.empty((n, d), dtype=torch.bfloat16, device="cuda")
+        y = torch.empty_like(recv)
+        ws = moe.ep_workspace(cfg, n)
+        remote_bytes = (n - n_self) * d * 2
+
+        def run(sched, chunks=1):
+            moe.moe_ep_expert_ffn(cfg, sched, n, x, T, xp, T, rt, off, se, gate_up, down, recv, y, ws,
+                                  chunks=chunks, link_workgroups=EP_LINK_WORKGROUPS, gemm_workgroups=gemm_wg,
+                                  s_compute=s_c, s_link=link)
+
+        link_ms = timed(lambda: moe.moe_ep_copy_rows(cfg, moe.MOE_EP_REMOTE, n, xp, T, rt, off, se, 0, E, recv,
+                                                     max_workgroups=EP_LINK_WORKGROUPS, stream=s_c))
+        link_gbs.append(remote_bytes / (link_ms / 1e3) / 1e9)
+        ffn_all = timed(lambda: moe.moe_expert_ffn_segments(cfg, n, recv, off, None, 0, E, gate_up, down, y, ws,
+                                                            stream=s_c))
+        ffn_two = timed(lambda: (moe.moe_expert_ffn_segments(cfg, n, recv, off, se, 0, E, gate_up, down, y, ws,
+                                                             stream=s_c),
+                                 moe.moe_expert_ffn_segments(cfg, n, recv, se, off[1:], 0, E, gate_up, down, y, ws,
+                                                             stream=s_c)))
+        seq = timed(lambda: run("sequential"))
+        split = timed(lambda: run("self_remote"))
+        chunked = {c: timed(lambda c=c: run("expert_chunks", c)) for c in EP_CHUNKS}
+        best_c = min(chunked, key=chunked.get)
+        ratios.append(dict(
+            ratio=f"{r}:1", rows=n, self_rows=n_self, remote_rows=n - n_self,
+            remote_mb=round(remote_bytes / 1e6, 1), link_ms=round(link_ms, 3),
+            ffn_all_rows_ms=round(ffn_all, 3), ffn_self_then_remote_ms=round(ffn_two, 3),
+            sequential_ms=round(seq, 3), self_remote_ms=round(split, 3),
+            expert_chunks_ms={str(c): round(v, 3) for c, v in chunked.items()},
+            self_remote_speedup=round(seq / split, 3), expert_chunks_speedup=round(seq / chunked[best_c], 3),
+            best_chunks=best_c))
+        del recv, y, ws, rt
+        torch.cuda.empty_cache()
+    return dict(local_experts=E, tokens_per_rank=T, link_workgroups=EP_LINK_WORKGROUPS,
+                link_gbs=round(sum(link_gbs) / len(link_gbs), 1), gemm_workgroups=gemm_wg, ratios=ratios,
+                note="one GPU of a two-GPU expert-parallel pair; the exchange of remote rows is a copy limited to "
+                     "link_workgroups workgroups on its own stream; speedups are over the sequential schedule")
+
+
 def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens: int = 64,
-                 ffn_only: bool = False, layout: str = "packed", multilayer: tuple = (), int8: bool = False):
+                 ffn_only: bool = False, layout: str = "packed", multilayer: tuple = (), int8: bool = False,
+                 ep: bool = False):
     import numpy as np
     import torch
 
@@ -216,8 +317,14 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
                   note="layer with int8 tokens runs the shared expert outside the routed GEMMs")
         del codes, scales, ws8
 
+    ep_res = None
+    if ep and cfg.packed and not ffn_only and p["E"] % 2 == 0 and p["dtype"] == "bf16":
+        log(f"[bench] {name}: expert-parallel receive side, ratios {inputs.EP_RATIOS}")
+        ep_res = ep_split(p, t["x"], w_ffn[0], w_ffn[2], steps, warmup)
+
     res = dict(
         name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms, int8_tokens=q8,
+        ep_split=ep_res,
         counts_max_over_mean=float(counts.max() / counts.mean()), empty_experts=int((counts == 0).sum()),
         layer_hbm_frac=alg["layer_bytes"] / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
         layer_mfma_frac=alg["layer_flops"] / (ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12),
@@ -317,7 +424,7 @@ def main():
         del src, dst
     main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_tokens,
                             args.ffn_only, args.layout, multilayer=() if args.no_extra else (1, 4, 16),
-                            int8=not args.no_extra)
+                            int8=not args.no_extra, ep=not args.no_extra)
     if args.ffn_only:
         print(json.dumps(dict(workload=args.workload, expert_ffn_ms=main_res["ffn_ms"],
                               expert_ffn_gbs=main_res["ffn_gbs"], expert_ffn_tflops=main_res["ffn_tflops"])))
@@ -385,6 +492,8 @@ def main():
     if r["multilayer_ms_per_layer"]:
         out["multilayer"] = {"ms_per_layer": {str(L): round(v, 4) for L, v in r["multilayer_ms_per_layer"].items()},
                              "note": "L layer calls back to back on the same input and weights, each into its own output"}
+    if r["ep_split"]:
+        out["ep_split"] = r["ep_split"]
     if extra:
         out["extra"] = extra
     print(json.dumps(out), flush=True)

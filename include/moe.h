@@ -286,6 +286,101 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
 int moe_pack_weights(const moe_config_t* cfg, const void* w_gate, const void* w_up, const void* w_down,
                      void* gate_up_packed, void* down_packed, hipStream_t stream);
 
+/* ---- Receive side of expert parallelism (one GPU's share) --------------
+ *
+ * The paper's MoE workload (App. M; §4.3, Table 5) spreads the experts over
+ * GPUs: the dispatch exchange brings each GPU the token rows routed to its
+ * experts, its own tokens' rows ("self", available at once) and the peers'
+ * ("remote", available once the exchange has delivered them). The calls
+ * below run that receive side on one GPU, with the exchange's delivery of
+ * the remote rows emulated by a copy whose rate is set by the workgroups it
+ * may use (it runs on its own stream next to the expert GEMMs).
+ *
+ * Receive buffer: n_rows rows of d elements (cfg->dtype), one per (token,
+ * local expert) assignment, grouped by local expert e in [0, cfg->E):
+ *   rows [offsets[e], self_end[e])      self rows:   row of x_self
+ *   rows [self_end[e], offsets[e + 1])  remote rows: row of x_peer
+ * with row_token[r] the row's token in its source. offsets [E+1] and
+ * self_end [E] are device int32 arrays, row_token [n_rows]. All three calls
+ * need packed bf16 weights (moe_pack_weights, the E local experts) and
+ * unquantized tokens; the workspace is moe_workspace_size(cfg,
+ * ceil(n_rows / k)) bytes. Malformed offsets or indices are clamped
+ * (unspecified rows, never an access out of bounds).
+ */
+typedef enum { MOE_EP_SELF = 0, MOE_EP_REMOTE = 1 } moe_ep_source_t;
+
+/* moe_ep_plan — the receive buffer's layout for the local experts, global
+ * experts [e_first, e_first + cfg->E), from this GPU's dispatch and the
+ * peer's (moe_dispatch over the global experts: offsets [>= e_first+E+1],
+ * sorted_token [assignments]): expert e's rows are this GPU's rows of that
+ * expert then the peer's, each in its dispatch order (token ascending):
+ *   offsets[e]  = (self_offsets[g] - self_offsets[e_first])
+ *               + (peer_offsets[g] - peer_offsets[e_first]),  g = e_first + e
+ *   self_end[e] = offsets[e] + self count of g
+ *   row_token   : the tokens in that order.
+ * Stands in for the exchange of per-expert counts between GPUs. Outputs:
+ * offsets [E+1], self_end [E], row_token [capacity] (rows past the capacity
+ * are not written). */
+int moe_ep_plan(const moe_config_t* cfg, int32_t e_first, const int32_t* self_offsets, const int32_t* self_sorted_token,
+                int32_t self_assignments, const int32_t* peer_offsets, const int32_t* peer_sorted_token,
+                int32_t peer_assignments, int32_t* row_token, int32_t capacity, int32_t* offsets, int32_t* self_end,
+                hipStream_t stream);
+
+/* moe_ep_copy_rows — fills the rows of one source (moe_ep_source_t) of the
+ * experts [e_begin, e_end): recv[r] = x_src[row_token[r]].
+ *  x_src : [src_tokens][d]; recv : [n_rows][d].
+ *  max_workgroups > 0 caps the copy's workgroups (the emulated link's rate;
+ *  0: as many as fill the device). */
+int moe_ep_copy_rows(const moe_config_t* cfg, int32_t source, int32_t n_rows, const void* x_src, int32_t src_tokens,
+                     const int32_t* row_token, const int32_t* offsets, const int32_t* self_end, int32_t e_begin,
+                     int32_t e_end, void* recv, int32_t max_workgroups, hipStream_t stream);
+
+/* moe_expert_ffn_segments — moe_expert_ffn over row segments of a receive
+ * buffer (App. M step 3), for experts e in [e_begin, e_end) and rows r in
+ * [seg_begin[e], seg_end[e]) (seg_end NULL: [seg_begin[e], seg_begin[e+1]),
+ * seg_begin then holding E+1 entries; index arrays need 4-byte alignment):
+ *   h[r] = silu(x[r] · w_gate[e]ᵀ) * (x[r] · w_up[e]ᵀ),   y[r] = h[r] · w_down[e]ᵀ
+ * x, y : [n_rows][d] (no gather; rows outside the segments are untouched).
+ * max_workgroups > 0 caps the GEMMs' workgroups (leaving compute units to
+ * kernels on other streams); 0: one per compute unit. */
+int moe_expert_ffn_segments(const moe_config_t* cfg, int32_t n_rows, const void* x, const int32_t* seg_begin,
+                            const int32_t* seg_end, int32_t e_begin, int32_t e_end, const void* w_gate_up,
+                            const void* w_down, void* y, int32_t max_workgroups, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Order of the receive side's work (§4.3: DeepEP's sequential phases vs the
+ * two-stream pipeline the paper's search found). */
+typedef enum {
+  MOE_EP_SEQUENTIAL = 0,   /* all rows received, then one FFN over them */
+  MOE_EP_SELF_REMOTE = 1,  /* the self rows' FFN while the remote rows arrive, then the
+                              remote rows' FFN once all of them are in (the paper's split;
+                              every expert's weights are streamed twice) */
+  MOE_EP_EXPERT_CHUNKS = 2 /* the remote rows arrive by expert range; each range's FFN,
+                              self and remote rows together, starts once its rows are in
+                              (every expert's weights streamed once) */
+} moe_ep_schedule_t;
+
+typedef struct {
+  int32_t schedule;        /* moe_ep_schedule_t                                        */
+  int32_t chunks;          /* MOE_EP_EXPERT_CHUNKS: expert ranges, 1 .. min(16, E)     */
+  int32_t link_workgroups; /* workgroups of the remote rows' copy (0: no cap)          */
+  int32_t gemm_workgroups; /* workgroups of the GEMMs that run while rows still arrive
+                              (0: one per compute unit)                                */
+} moe_ep_options_t;
+
+/* moe_ep_expert_ffn — the receive side in one call: the self rows copied
+ * into recv on s_compute, the remote rows on s_link (the exchange), and the
+ * FFN of every row into y on s_compute, ordered by opt->schedule; s_compute
+ * waits for s_link's work before the call's last kernel, so everything is
+ * complete when s_compute reaches the end of the call. s_link NULL (or equal
+ * to s_compute): one stream. y[r] is the same for every schedule.
+ *  x_self : [self_tokens][d]; x_peer : [peer_tokens][d];
+ *  recv, y : [n_rows][d] out. */
+int moe_ep_expert_ffn(const moe_config_t* cfg, const moe_ep_options_t* opt, int32_t n_rows, const void* x_self,
+                      int32_t self_tokens, const void* x_peer, int32_t peer_tokens, const int32_t* row_token,
+                      const int32_t* offsets, const int32_t* self_end, const void* w_gate_up, const void* w_down,
+                      void* recv, void* y, void* ws, size_t ws_bytes, hipStream_t s_compute, hipStream_t s_link);
+
 /* Static text for a moe_status_t. */
 const char* moe_status_string(int status);
 /* Message of the last failing call on this thread ("" if none). */

@@ -140,6 +140,14 @@ int need(const void* p, const char* name) {
   return MOE_OK;
 }
 
+// int32 index arrays of the expert-parallel calls: non-null and 4-byte
+// aligned (they may start inside another array, e.g. offsets + 1).
+int need_i32(const void* p, const char* name) {
+  if (!p) return fail(MOE_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  if (reinterpret_cast<uintptr_t>(p) & 3u) return fail(MOE_ERR_INVALID_ARG, std::string(name) + " is not 4-byte aligned");
+  return MOE_OK;
+}
+
 #define MOE_CHECK(expr)            \
   do {                             \
     const int _s = (expr);         \
@@ -239,10 +247,13 @@ struct FusedShared {
 // the shared expert over all a_rows tokens rides along as an extra group.
 // queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path.
 // x_scales: x holds int8 codes of rows with these fp32 scales (packed only).
+// seg_end, max_wg (packed only): group g owns rows [offsets[g], seg_end[g]);
+// at most max_wg workgroups per GEMM (0: one per compute unit).
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
-                   int32_t* queues = nullptr, const float* x_scales = nullptr) {
+                   int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
+                   int32_t max_wg = 0) {
   if (packed && queues) {
     const hipError_t e = moe::launch_queue_reset(queues, 16, s);
     if (e != hipSuccess) return e;
@@ -268,6 +279,8 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   }
   up.tile_queue = queues;
   up.a_scale = x_scales;
+  up.seg_end = seg_end;
+  up.max_wg = max_wg;
   hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
   if (e != hipSuccess) return e;
   moe::GemmProblem down{};
@@ -288,6 +301,8 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
     down.x_rows = a_rows;
   }
   down.tile_queue = queues ? queues + 8 : nullptr;
+  down.seg_end = seg_end;
+  down.max_wg = max_wg;
   return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
@@ -325,6 +340,78 @@ hipError_t layer_events(StreamEvents** out) {
   }
   *out = &se;
   return hipSuccess;
+}
+
+// Events per (thread, device) of moe_ep_expert_ffn: the fork and one per
+// transferred expert range.
+constexpr int kEpMaxChunks = 16;
+struct EpEvents {
+  hipEvent_t fork = nullptr;
+  hipEvent_t chunk[kEpMaxChunks] = {};
+};
+
+hipError_t ep_events(EpEvents** out) {
+  thread_local EpEvents ev[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  EpEvents& se = ev[dev];
+  if (!se.fork) {
+    for (int i = 0; i < kEpMaxChunks; ++i)
+      if ((e = hipEventCreateWithFlags(&se.chunk[i], hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&se.fork, hipEventDisableTiming)) != hipSuccess) return e;
+  }
+  *out = &se;
+  return hipSuccess;
+}
+
+// The receive buffer's checks shared by the expert-parallel entry points:
+// a packed bf16 config, and n_rows rows whose workspace is that of
+// ceil(n_rows / k) tokens.
+int validate_ep(const moe_config_t* c, int32_t n_rows, int32_t* tokens_out) {
+  if (!c) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
+  if (n_rows < 0) return fail(MOE_ERR_INVALID_ARG, "n_rows < 0");
+  if (c->k <= 0) return fail(MOE_ERR_INVALID_ARG, "k must be positive");
+  const int32_t T = (int32_t)(((int64_t)n_rows + c->k - 1) / c->k);
+  MOE_CHECK(validate(c, T));
+  if (c->weight_layout != MOE_LAYOUT_PACKED || c->token_quant != MOE_QUANT_NONE)
+    return fail(MOE_ERR_UNSUPPORTED, "the expert-parallel calls need packed bf16 weights and unquantized tokens");
+  if ((int64_t)n_rows * c->d * 2 > (int64_t)UINT32_MAX)
+    return fail(MOE_ERR_UNSUPPORTED, "n_rows*d must be below 2^31 elements");
+  *tokens_out = T;
+  return MOE_OK;
+}
+
+// FFN of experts [e0, e1) over row segments of x (no gather).
+hipError_t run_ffn_segments(const moe_config_t& c, int32_t n_rows, const void* x, const int32_t* seg_begin,
+                            const int32_t* seg_end, int32_t e0, int32_t e1, const void* w_gate_up, const void* w_down,
+                            void* y, int32_t max_wg, char* ws, const Layout& L, hipStream_t s) {
+  if (e1 <= e0 || n_rows == 0) return hipSuccess;
+  // packed bf16: an expert's gate+up block is 2*I*d elements, its down block d*I
+  const char* wgu = static_cast<const char*>(w_gate_up) + (size_t)e0 * 2 * c.I * c.d * 2;
+  const char* wd = static_cast<const char*>(w_down) + (size_t)e0 * c.d * c.I * 2;
+  return run_ffn(c, n_rows, n_rows, e1 - e0, c.I, x, nullptr, seg_begin + e0, wgu, nullptr, wd, ws + L.h, y, s, true,
+                 nullptr, reinterpret_cast<int32_t*>(ws + L.queues), nullptr, seg_end ? seg_end + e0 : nullptr,
+                 max_wg);
+}
+
+hipError_t run_ep_copy(const moe_config_t& c, int32_t mode, int32_t n_rows, const void* src, int32_t src_tokens,
+                       const int32_t* row_token, const int32_t* offsets, const int32_t* self_end, int32_t e0,
+                       int32_t e1, void* recv, int32_t max_wg, hipStream_t s) {
+  moe::EpCopyParams p{};
+  p.src = src;
+  p.src_rows = src_tokens;
+  p.row_token = row_token;
+  p.offsets = offsets;
+  p.self_end = self_end;
+  p.e0 = e0;
+  p.e1 = e1;
+  p.mode = mode;
+  p.n_rows = n_rows;
+  p.row_bytes = c.d * (int32_t)esize(c);
+  p.dst = recv;
+  return moe::launch_ep_copy(p, max_wg, s);
 }
 
 }  // namespace
@@ -569,6 +656,166 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     }
   }
   if ((e = run_combine(c, T, y, inv, tw, shared, out, s_main)) != hipSuccess) return hip_fail(e, "combine");
+  return MOE_OK;
+}
+
+int moe_ep_plan(const moe_config_t* cfg, int32_t e_first, const int32_t* self_offsets, const int32_t* self_sorted_token,
+                int32_t self_assignments, const int32_t* peer_offsets, const int32_t* peer_sorted_token,
+                int32_t peer_assignments, int32_t* row_token, int32_t capacity, int32_t* offsets, int32_t* self_end,
+                hipStream_t stream) {
+  if (!cfg) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
+  if (cfg->E <= 0 || cfg->E > 256) return fail(MOE_ERR_INVALID_ARG, "local experts must be in [1, 256]");
+  if (e_first < 0) return fail(MOE_ERR_INVALID_ARG, "e_first < 0");
+  if (self_assignments < 0 || peer_assignments < 0 || capacity < 0)
+    return fail(MOE_ERR_INVALID_ARG, "negative size");
+  MOE_CHECK(need_i32(self_offsets, "self_offsets"));
+  MOE_CHECK(need_i32(peer_offsets, "peer_offsets"));
+  if (self_assignments > 0) MOE_CHECK(need_i32(self_sorted_token, "self_sorted_token"));
+  if (peer_assignments > 0) MOE_CHECK(need_i32(peer_sorted_token, "peer_sorted_token"));
+  if (capacity > 0) MOE_CHECK(need_i32(row_token, "row_token"));
+  MOE_CHECK(need_i32(offsets, "offsets"));
+  MOE_CHECK(need_i32(self_end, "self_end"));
+  moe::EpPlanParams p{};
+  p.self_offsets = self_offsets;
+  p.self_sorted = self_sorted_token;
+  p.self_total = self_assignments;
+  p.peer_offsets = peer_offsets;
+  p.peer_sorted = peer_sorted_token;
+  p.peer_total = peer_assignments;
+  p.e_first = e_first;
+  p.e_count = cfg->E;
+  p.capacity = capacity;
+  p.row_token = row_token;
+  p.offsets = offsets;
+  p.self_end = self_end;
+  const hipError_t e = moe::launch_ep_plan(p, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "receive plan");
+}
+
+int moe_ep_copy_rows(const moe_config_t* cfg, int32_t source, int32_t n_rows, const void* x_src, int32_t src_tokens,
+                     const int32_t* row_token, const int32_t* offsets, const int32_t* self_end, int32_t e_begin,
+                     int32_t e_end, void* recv, int32_t max_workgroups, hipStream_t stream) {
+  int32_t T = 0;
+  MOE_CHECK(validate_ep(cfg, n_rows, &T));
+  if (source != MOE_EP_SELF && source != MOE_EP_REMOTE) return fail(MOE_ERR_INVALID_ARG, "unknown row source");
+  if (e_begin < 0 || e_end > cfg->E || e_begin > e_end) return fail(MOE_ERR_INVALID_ARG, "bad expert range");
+  MOE_CHECK(need_i32(row_token, "row_token"));
+  MOE_CHECK(need_i32(offsets, "offsets"));
+  MOE_CHECK(need_i32(self_end, "self_end"));
+  MOE_CHECK(need(recv, "recv"));
+  if (src_tokens < 0) return fail(MOE_ERR_INVALID_ARG, "src_tokens < 0");
+  if (src_tokens > 0) MOE_CHECK(need(x_src, "x_src"));
+  if (n_rows == 0 || e_begin == e_end || src_tokens == 0) return MOE_OK;
+  const hipError_t e = run_ep_copy(*cfg, source, n_rows, x_src, src_tokens, row_token, offsets, self_end, e_begin,
+                                   e_end, recv, max_workgroups, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "row copy");
+}
+
+int moe_expert_ffn_segments(const moe_config_t* cfg, int32_t n_rows, const void* x, const int32_t* seg_begin,
+                            const int32_t* seg_end, int32_t e_begin, int32_t e_end, const void* w_gate_up,
+                            const void* w_down, void* y, int32_t max_workgroups, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  int32_t T = 0;
+  MOE_CHECK(validate_ep(cfg, n_rows, &T));
+  if (e_begin < 0 || e_end > cfg->E || e_begin > e_end) return fail(MOE_ERR_INVALID_ARG, "bad expert range");
+  MOE_CHECK(need(x, "x"));
+  MOE_CHECK(need_i32(seg_begin, "seg_begin"));
+  if (seg_end) MOE_CHECK(need_i32(seg_end, "seg_end"));
+  MOE_CHECK(need(w_gate_up, "w_gate_up"));
+  MOE_CHECK(need(w_down, "w_down"));
+  MOE_CHECK(need(y, "y"));
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  if (n_rows == 0 || e_begin == e_end) return MOE_OK;
+  const hipError_t e = run_ffn_segments(*cfg, n_rows, x, seg_begin, seg_end, e_begin, e_end, w_gate_up, w_down, y,
+                                        max_workgroups, static_cast<char*>(ws), make_layout(*cfg, T), stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
+}
+
+int moe_ep_expert_ffn(const moe_config_t* cfg, const moe_ep_options_t* opt, int32_t n_rows, const void* x_self,
+                      int32_t self_tokens, const void* x_peer, int32_t peer_tokens, const int32_t* row_token,
+                      const int32_t* offsets, const int32_t* self_end, const void* w_gate_up, const void* w_down,
+                      void* recv, void* y, void* ws, size_t ws_bytes, hipStream_t s_compute, hipStream_t s_link) {
+  int32_t T = 0;
+  MOE_CHECK(validate_ep(cfg, n_rows, &T));
+  if (!opt) return fail(MOE_ERR_INVALID_ARG, "options are NULL");
+  const moe_ep_options_t o = *opt;
+  if (o.schedule != MOE_EP_SEQUENTIAL && o.schedule != MOE_EP_SELF_REMOTE && o.schedule != MOE_EP_EXPERT_CHUNKS)
+    return fail(MOE_ERR_INVALID_ARG, "unknown schedule");
+  if (o.schedule == MOE_EP_EXPERT_CHUNKS && (o.chunks < 1 || o.chunks > kEpMaxChunks || o.chunks > cfg->E))
+    return fail(MOE_ERR_INVALID_ARG, "chunks must be in [1, min(16, E)]");
+  if (o.link_workgroups < 0 || o.gemm_workgroups < 0) return fail(MOE_ERR_INVALID_ARG, "negative workgroup cap");
+  if (self_tokens < 0 || peer_tokens < 0) return fail(MOE_ERR_INVALID_ARG, "token counts < 0");
+  if (self_tokens > 0) MOE_CHECK(need(x_self, "x_self"));
+  if (peer_tokens > 0) MOE_CHECK(need(x_peer, "x_peer"));
+  MOE_CHECK(need_i32(row_token, "row_token"));
+  MOE_CHECK(need_i32(offsets, "offsets"));
+  MOE_CHECK(need_i32(self_end, "self_end"));
+  MOE_CHECK(need(w_gate_up, "w_gate_up"));
+  MOE_CHECK(need(w_down, "w_down"));
+  MOE_CHECK(need(recv, "recv"));
+  MOE_CHECK(need(y, "y"));
+  MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
+  if (n_rows == 0) return MOE_OK;
+
+  const moe_config_t& c = *cfg;
+  const Layout L = make_layout(c, T);
+  char* const w = static_cast<char*>(ws);
+  const bool two = s_link && s_link != s_compute;
+  hipStream_t const sl = two ? s_link : s_compute;
+  EpEvents* ev = nullptr;
+  hipError_t e;
+  if ((e = ep_events(&ev)) != hipSuccess) return hip_fail(e, "event create");
+  if (two) {  // the transfer may start once the caller's inputs are ready on s_compute
+    if ((e = hipEventRecord(ev->fork, s_compute)) != hipSuccess) return hip_fail(e, "event record");
+    if ((e = hipStreamWaitEvent(sl, ev->fork, 0)) != hipSuccess) return hip_fail(e, "stream wait");
+  }
+  auto copy = [&](int mode, int e0, int e1, int max_wg, hipStream_t s) {
+    const void* src = mode == MOE_EP_SELF ? x_self : x_peer;
+    const int32_t nsrc = mode == MOE_EP_SELF ? self_tokens : peer_tokens;
+    if (nsrc == 0) return hipSuccess;
+    return run_ep_copy(c, mode, n_rows, src, nsrc, row_token, offsets, self_end, e0, e1, recv, max_wg, s);
+  };
+  auto ffn = [&](const int32_t* b, const int32_t* en, int e0, int e1, int max_wg) {
+    return run_ffn_segments(c, n_rows, recv, b, en, e0, e1, w_gate_up, w_down, y, max_wg, w, L, s_compute);
+  };
+  auto join = [&](hipEvent_t done) -> hipError_t {  // s_compute waits for the transfer up to here
+    if (!two) return hipSuccess;
+    hipError_t r = hipEventRecord(done, sl);
+    return r != hipSuccess ? r : hipStreamWaitEvent(s_compute, done, 0);
+  };
+  const int E = c.E;
+  switch (o.schedule) {
+    case MOE_EP_SEQUENTIAL:
+      // every row in, then one FFN over all of them
+      if ((e = copy(MOE_EP_REMOTE, 0, E, o.link_workgroups, sl)) != hipSuccess) return hip_fail(e, "transfer");
+      if ((e = copy(MOE_EP_SELF, 0, E, 0, s_compute)) != hipSuccess) return hip_fail(e, "self copy");
+      if ((e = join(ev->chunk[0])) != hipSuccess) return hip_fail(e, "stream join");
+      if ((e = ffn(offsets, nullptr, 0, E, 0)) != hipSuccess) return hip_fail(e, "expert FFN");
+      break;
+    case MOE_EP_SELF_REMOTE:
+      // the self rows' FFN runs while the remote rows arrive; the remote
+      // rows' FFN starts when all of them are in
+      if ((e = copy(MOE_EP_REMOTE, 0, E, o.link_workgroups, sl)) != hipSuccess) return hip_fail(e, "transfer");
+      if ((e = copy(MOE_EP_SELF, 0, E, 0, s_compute)) != hipSuccess) return hip_fail(e, "self copy");
+      if ((e = ffn(offsets, self_end, 0, E, o.gemm_workgroups)) != hipSuccess) return hip_fail(e, "self FFN");
+      if ((e = join(ev->chunk[0])) != hipSuccess) return hip_fail(e, "stream join");
+      if ((e = ffn(self_end, offsets + 1, 0, E, 0)) != hipSuccess) return hip_fail(e, "remote FFN");
+      break;
+    default: {
+      // the remote rows arrive by expert range; each range's FFN (its self
+      // and remote rows in one pass over its weights) starts when its rows
+      // are in
+      const int C = o.chunks;
+      if ((e = copy(MOE_EP_SELF, 0, E, 0, s_compute)) != hipSuccess) return hip_fail(e, "self copy");
+      for (int i = 0; i < C; ++i) {
+        const int e0 = (int)((int64_t)E * i / C), e1 = (int)((int64_t)E * (i + 1) / C);
+        if ((e = copy(MOE_EP_REMOTE, e0, e1, o.link_workgroups, sl)) != hipSuccess) return hip_fail(e, "transfer");
+        if ((e = join(ev->chunk[i])) != hipSuccess) return hip_fail(e, "stream join");
+        if ((e = ffn(offsets, nullptr, e0, e1, i + 1 < C ? o.gemm_workgroups : 0)) != hipSuccess)
+          return hip_fail(e, "expert FFN");
+      }
+    }
+  }
   return MOE_OK;
 }
 

@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       int c = p.M;
       if (p.offsets) {
         const int lo = min(max(p.offsets[tid], 0), p.M);
-        c = min(max(p.offsets[tid + 1], lo), p.M) - lo;
+        c = min(max(p.seg_end ? p.seg_end[tid] : p.offsets[tid + 1], lo), p.M) - lo;
       }
       mt = (c + kMaxRows - 1) / kMaxRows;
     }
@@ -251,7 +251,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       const int pass = local % passes;
       nt = local / passes;
       const int gbeg = p.offsets ? min(max(p.offsets[e], 0), p.M) : 0;
-      const int gend = p.offsets ? min(max(p.offsets[e + 1], gbeg), p.M) : p.M;
+      const int gend = p.offsets ? min(max(p.seg_end ? p.seg_end[e] : p.offsets[e + 1], gbeg), p.M) : p.M;
       a_base = p.A;
       a_rows = p.a_rows;
       gather = p.gather;
@@ -587,6 +587,7 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
   const long long upper = passes_upper * (p.N / tcols);
   if (upper <= 0) return hipSuccess;
   long long grid = device_cu_count();
+  if (p.max_wg > 0 && grid > p.max_wg) grid = p.max_wg;
   if (grid > upper) grid = upper;
   if (grid >= 8) grid -= grid % 8;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, s, p);

@@ -68,6 +68,13 @@ struct GemmProblem {
   // gate and up sums are multiplied by its row's scale before the SwiGLU.
   // The extra group must be empty (x_rows == 0). nullptr: A is bf16.
   const float* a_scale;
+  // Weight-streaming kernel only: group g owns rows [offsets[g], seg_end[g])
+  // instead of [offsets[g], offsets[g+1]) (nullptr: adjacent segments), so a
+  // call can cover part of every group's rows.
+  const int32_t* seg_end;
+  // Weight-streaming kernel only: at most this many workgroups (0: one per
+  // compute unit), leaving compute units to kernels on other streams.
+  int32_t max_wg;
 };
 
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
@@ -131,6 +138,39 @@ hipError_t launch_combine(const CombineParams& p, bool bf16, hipStream_t s);
 // to +-127, scale[t] = max_c |x[t][c]| / 127 (0 and codes 0 for a zero row).
 // x bf16 [T][d], d % 64 == 0; codes int8 [T][d]; scales fp32 [T].
 hipError_t launch_quantize(const void* x, int8_t* codes, float* scales, int T, int d, hipStream_t s);
+
+// Receive side of expert parallelism: fills the self (mode 0) or remote
+// (mode 1) rows of experts [e0, e1) of a receive buffer whose expert e owns
+// rows [offsets[e], offsets[e+1]), self rows below self_end[e]:
+// dst[r] = src[row_token[r]] (rows of row_bytes bytes, a multiple of 16).
+// Indices are clamped into range. max_wg > 0 limits the workgroups.
+struct EpCopyParams {
+  const void* src;  // [src_rows][row_bytes]
+  int32_t src_rows;
+  const int32_t* row_token;  // [n_rows]
+  const int32_t* offsets;    // [E+1]
+  const int32_t* self_end;   // [E]
+  int32_t e0, e1, mode, n_rows, row_bytes;
+  void* dst;  // [n_rows][row_bytes]
+};
+hipError_t launch_ep_copy(const EpCopyParams& p, int max_wg, hipStream_t s);
+// Receive-buffer layout of local experts [e_first, e_first + e_count) from
+// this GPU's and the peer's dispatch (offsets over the global experts and
+// the expert-sorted token lists): offsets [e_count+1], self_end [e_count],
+// row_token [capacity] (rows past the capacity are not written).
+struct EpPlanParams {
+  const int32_t* self_offsets;
+  const int32_t* self_sorted;
+  int32_t self_total;
+  const int32_t* peer_offsets;
+  const int32_t* peer_sorted;
+  int32_t peer_total;
+  int32_t e_first, e_count, capacity;
+  int32_t* row_token;
+  int32_t* offsets;
+  int32_t* self_end;
+};
+hipError_t launch_ep_plan(const EpPlanParams& p, hipStream_t s);
 
 // Number of compute units of the current device (cached per device).
 int device_cu_count();

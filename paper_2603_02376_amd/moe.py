@@ -23,6 +23,8 @@ MOE_F32, MOE_BF16 = 0, 1
 MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_LAYOUT_ROWMAJOR, MOE_LAYOUT_PACKED = 0, 1
 MOE_QUANT_NONE, MOE_QUANT_INT8 = 0, 1
+MOE_EP_SELF, MOE_EP_REMOTE = 0, 1
+EP_SCHEDULES = {"sequential": 0, "self_remote": 1, "expert_chunks": 2}
 STATUS = {0: "MOE_OK", -1: "MOE_ERR_INVALID_ARG", -2: "MOE_ERR_UNSUPPORTED",
           -3: "MOE_ERR_WORKSPACE", -4: "MOE_ERR_HIP"}
 
@@ -39,6 +41,11 @@ class moe_config_t(ctypes.Structure):
                 ("n_shared", ctypes.c_int32), ("I_shared", ctypes.c_int32), ("score", ctypes.c_int32),
                 ("renorm", ctypes.c_int32), ("route_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("weight_layout", ctypes.c_int32), ("token_quant", ctypes.c_int32)]
+
+
+class moe_ep_options_t(ctypes.Structure):
+    _fields_ = [("schedule", ctypes.c_int32), ("chunks", ctypes.c_int32), ("link_workgroups", ctypes.c_int32),
+                ("gemm_workgroups", ctypes.c_int32)]
 
 
 class moe_layer_debug_t(ctypes.Structure):
@@ -61,6 +68,12 @@ _SIGS = {
     "moe_layer": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ,
                                  _VP, _VP, ctypes.POINTER(moe_layer_debug_t)]),
     "moe_pack_weights": (ctypes.c_int, [_CFG, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "moe_ep_plan": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _I32, _VP, _VP, _I32, _VP, _I32, _VP, _VP, _VP]),
+    "moe_ep_copy_rows": (ctypes.c_int, [_CFG, _I32, _I32, _VP, _I32, _VP, _VP, _VP, _I32, _I32, _VP, _I32, _VP]),
+    "moe_expert_ffn_segments": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _I32, _I32, _VP, _VP, _VP, _I32, _VP,
+                                               _SZ, _VP]),
+    "moe_ep_expert_ffn": (ctypes.c_int, [_CFG, ctypes.POINTER(moe_ep_options_t), _I32, _VP, _I32, _VP, _I32, _VP,
+                                         _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP, _VP]),
     "moe_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "moe_last_error": (ctypes.c_char_p, []),
     "moe_version": (ctypes.c_char_p, []),
@@ -309,6 +322,76 @@ def pack_shared_weights(cfg: MoeConfig, ws_gate, ws_up, ws_down):
     weights, packed as a single expert); returns (gate_up_packed, down_packed)."""
     one = dataclasses.replace(cfg, E=1, k=1, n_groups=1, topk_groups=1, I=cfg.I_shared, n_shared=0, I_shared=0)
     return pack_weights(one, ws_gate.unsqueeze(0), ws_up.unsqueeze(0), ws_down.unsqueeze(0))
+
+
+# ---- receive side of expert parallelism (one GPU's share) -------------------
+
+def ep_workspace(cfg: MoeConfig, n_rows: int, device="cuda") -> torch.Tensor:
+    """Workspace of the expert-parallel calls for n_rows received rows."""
+    return alloc_workspace(cfg, -(-n_rows // cfg.k), device)
+
+
+def moe_ep_plan(cfg: MoeConfig, e_first, self_offsets, self_sorted_token, self_assignments, peer_offsets,
+                peer_sorted_token, peer_assignments, row_token, capacity, offsets, self_end, stream=None):
+    """Receive-buffer layout of the local experts (cfg.E of them, from global expert e_first)."""
+    c = cfg.c()
+    _check(lib().moe_ep_plan(ctypes.byref(c), e_first,
+                             _ptr(self_offsets, "self_offsets", torch.int32, e_first + cfg.E + 1),
+                             _ptr(self_sorted_token, "self_sorted_token", torch.int32, self_assignments),
+                             self_assignments,
+                             _ptr(peer_offsets, "peer_offsets", torch.int32, e_first + cfg.E + 1),
+                             _ptr(peer_sorted_token, "peer_sorted_token", torch.int32, peer_assignments),
+                             peer_assignments, _ptr(row_token, "row_token", torch.int32, capacity), capacity,
+                             _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                             _ptr(self_end, "self_end", torch.int32, cfg.E), _stream(stream)))
+
+
+def moe_ep_copy_rows(cfg: MoeConfig, source, n_rows, x_src, src_tokens, row_token, offsets, self_end, e_begin, e_end,
+                     recv, max_workgroups=0, stream=None):
+    """Fill the self (source 0) or remote (1) rows of experts [e_begin, e_end)."""
+    c = cfg.c()
+    dt = cfg.torch_dtype
+    _check(lib().moe_ep_copy_rows(ctypes.byref(c), int(source), n_rows, _ptr(x_src, "x_src", dt, src_tokens * cfg.d),
+                                  src_tokens, _ptr(row_token, "row_token", torch.int32, n_rows),
+                                  _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                                  _ptr(self_end, "self_end", torch.int32, cfg.E), e_begin, e_end,
+                                  _ptr(recv, "recv", dt, n_rows * cfg.d), int(max_workgroups), _stream(stream)))
+
+
+def moe_expert_ffn_segments(cfg: MoeConfig, n_rows, x, seg_begin, seg_end, e_begin, e_end, w_gate_up, w_down, y, ws,
+                            max_workgroups=0, stream=None):
+    """FFN of experts [e_begin, e_end) over rows [seg_begin[e], seg_end[e]) of x
+    (seg_end None: [seg_begin[e], seg_begin[e+1]))."""
+    c = cfg.c()
+    wsz = cfg.E * cfg.I * cfg.d
+    _check(lib().moe_expert_ffn_segments(ctypes.byref(c), n_rows, _ptr(x, "x", torch.bfloat16, n_rows * cfg.d),
+                                         _ptr(seg_begin, "seg_begin", torch.int32, cfg.E + (seg_end is None)),
+                                         _ptr(seg_end, "seg_end", torch.int32, cfg.E), e_begin, e_end,
+                                         _ptr(w_gate_up, "w_gate_up", torch.bfloat16, 2 * wsz),
+                                         _ptr(w_down, "w_down", torch.bfloat16, wsz),
+                                         _ptr(y, "y", torch.bfloat16, n_rows * cfg.d), int(max_workgroups),
+                                         _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_ep_expert_ffn(cfg: MoeConfig, schedule: str, n_rows, x_self, self_tokens, x_peer, peer_tokens, row_token,
+                      offsets, self_end, w_gate_up, w_down, recv, y, ws, chunks=1, link_workgroups=0,
+                      gemm_workgroups=0, s_compute=None, s_link=None):
+    """The receive side in one call (schedule: "sequential", "self_remote" or "expert_chunks")."""
+    c = cfg.c()
+    o = moe_ep_options_t(EP_SCHEDULES[schedule], int(chunks), int(link_workgroups), int(gemm_workgroups))
+    wsz = cfg.E * cfg.I * cfg.d
+    _check(lib().moe_ep_expert_ffn(ctypes.byref(c), ctypes.byref(o), n_rows,
+                                   _ptr(x_self, "x_self", torch.bfloat16, self_tokens * cfg.d), self_tokens,
+                                   _ptr(x_peer, "x_peer", torch.bfloat16, peer_tokens * cfg.d), peer_tokens,
+                                   _ptr(row_token, "row_token", torch.int32, n_rows),
+                                   _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                                   _ptr(self_end, "self_end", torch.int32, cfg.E),
+                                   _ptr(w_gate_up, "w_gate_up", torch.bfloat16, 2 * wsz),
+                                   _ptr(w_down, "w_down", torch.bfloat16, wsz),
+                                   _ptr(recv, "recv", torch.bfloat16, n_rows * cfg.d),
+                                   _ptr(y, "y", torch.bfloat16, n_rows * cfg.d),
+                                   _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(s_compute),
+                                   _stream(s_link) if s_link is not None else None))
 
 
 def version() -> str:
