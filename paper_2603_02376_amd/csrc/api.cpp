@@ -32,14 +32,23 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 size_t esize(const moe_config_t& c) { return c.dtype == MOE_BF16 ? 2 : 4; }
 
-// K-split of the router GEMM (bf16 only): enough 32-row tiles x splits to
-// occupy ~512 workgroups, at least 4 k-steps of 64 per split. A function of
-// (T, d) only, so the workspace size does not depend on the device.
+// Row tile of the router GEMM: 64 rows from 2048 tokens up (half the
+// re-reads of the router weights of 32-row tiles, and one round of
+// workgroups), 32 below.
+constexpr int kGateM64Tokens = 2048;
+bool gate_m64(int32_t T) { return T >= kGateM64Tokens; }
+
+// K-split of the router GEMM (bf16 only): enough row tiles x splits to
+// occupy ~256 workgroups with 64-row tiles (~512 with 32-row tiles), at
+// least 4 k-steps of 64 per split. A function of (T, d) only, so the
+// workspace size does not depend on the device.
 int gate_splits(const moe_config_t& c, int32_t T) {
   if (c.dtype != MOE_BF16 || T <= 0) return 1;
-  const int mtiles = (T + 31) / 32;
+  const bool m64 = gate_m64(T);
+  const int mtiles = m64 ? (T + 63) / 64 : (T + 31) / 32;
+  const int target = m64 ? 256 : 512;
   const int nkt = c.d / 64;
-  int s = std::max(1, std::min(nkt / 4, (512 + mtiles - 1) / mtiles));
+  int s = std::max(1, std::min(nkt / 4, (target + mtiles - 1) / mtiles));
   const int q = (nkt + s - 1) / s;
   return (nkt + q - 1) / q;  // no empty split
 }
@@ -192,7 +201,7 @@ hipError_t run_gate_route(const moe_config_t& c, int32_t T, const void* x, const
     g.ldc = c.E;
     g.ksplit = splits;
     g.c_split_stride = (int64_t)T * c.E;
-    g.tile = moe::GEMM_TILE_SKINNY;
+    g.tile = gate_m64(T) ? moe::GEMM_TILE_M64 : moe::GEMM_TILE_SKINNY;
     const hipError_t e = run_gemm(c, g, moe::EPI_STORE, true, s);
     if (e != hipSuccess) return e;
   }

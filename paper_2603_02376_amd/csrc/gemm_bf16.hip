@@ -421,6 +421,7 @@ hipError_t launch_epi(const GemmProblem& p, int epi, bool out_f32, hipStream_t s
 hipError_t launch_gemm_bf16(const GemmProblem& p, int epi, bool out_f32, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.tile == GEMM_TILE_SKINNY) return launch_epi<32, 256, 64, 1, 4>(p, epi, out_f32, s);
+  if (p.tile == GEMM_TILE_M64) return launch_epi<64, 256, 64, 1, 4>(p, epi, out_f32, s);
   const int groups = p.offsets ? p.groups : 1;
   const double avg_rows = (double)p.M / groups;
   if (avg_rows >= 64) return launch_epi<256, 256, 64, 4, 2>(p, epi, out_f32, s);

@@ -16,7 +16,7 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 // Tile shape of the bf16 grouped GEMM: chosen from the rows per group, or
 // the skinny 32x256 shape (used by the router GEMM, whose N is the expert
 // count).
-enum GemmTile : int { GEMM_TILE_AUTO = 0, GEMM_TILE_SKINNY = 1 };
+enum GemmTile : int { GEMM_TILE_AUTO = 0, GEMM_TILE_SKINNY = 1, GEMM_TILE_M64 = 2 };
 
 // Epilogue of the grouped GEMM.
 enum GemmEpilogue : int {
