@@ -35,7 +35,9 @@ brute-force enumeration on tiny inputs, special cases that reduce to a dense
 SwiGLU or a dense softmax mixture, and invariants; the token quantization by
 hand-derived examples with exact power-of-two scales, its error bound and the
 quantized layer's reduction to the plain one on exactly representable
-tokens; the expert-parallel receive plan by hand-derived examples and
+tokens; the FP8 codes by hand-derived examples, the code table's defining
+properties and the same reduction; the expert-parallel receive plan by
+hand-derived examples and
 invariants, its FFN by its reduction to the single-GPU expert FFN). The layer
 as a whole has no value printed in the paper; it is pinned only through those
 pieces.
@@ -58,6 +60,9 @@ __all__ = [
     "layer_rows",
     "quantize_tokens",
     "dequantize_tokens",
+    "e4m3_values",
+    "quantize_tokens_fp8",
+    "dequantize_tokens_fp8",
     "ep_receive_plan",
     "ep_receive_ffn",
 ]
@@ -319,6 +324,78 @@ def dequantize_tokens(codes, scales) -> np.ndarray:
     return np.asarray(codes, dtype=np.float64) * np.asarray(scales, dtype=np.float64)[:, None]
 
 
+# FP8 (Table 5 names an FP8 quantize phase): the OCP E4M3 format, 1 sign,
+# 4 exponent (bias 7) and 3 mantissa bits; exponent field 0 holds the
+# subnormals m/8 * 2^-6, fields 1..15 the normals (1 + m/8) * 2^(e-7), and
+# only code 0x7F (with its sign) is NaN, so the largest finite value is 448.
+E4M3_MAX = 448.0
+
+
+def e4m3_values() -> np.ndarray:
+    """float64 [256]: the value of every E4M3 code (NaN for 0x7F and 0xFF)."""
+    out = np.empty(256)
+    for code in range(256):
+        sign = -1.0 if code & 0x80 else 1.0
+        e, m = (code >> 3) & 0xF, code & 0x7
+        if e == 0xF and m == 0x7:
+            out[code] = np.nan
+        elif e == 0:
+            out[code] = sign * (m / 8.0) * 2.0 ** -6
+        else:
+            out[code] = sign * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+    return out
+
+
+def _e4m3_encode(f) -> np.ndarray:
+    """Codes of float values: the nearest finite E4M3 magnitude (ties to the
+    even mantissa, which is the even code), magnitudes above 448 taken as 448,
+    and the sign bit of the value (so -0 and negatives that round to 0 give
+    0x80)."""
+    f = np.asarray(f, dtype=np.float64)
+    mags = e4m3_values()[:0x7F]            # codes 0x00..0x7E, increasing
+    a = np.minimum(np.abs(f), E4M3_MAX)
+    hi = np.clip(np.searchsorted(mags, a, side="left"), 0, 0x7E)   # first magnitude >= a
+    lo = np.clip(hi - 1, 0, 0x7E)
+    dlo, dhi = a - mags[lo], mags[hi] - a
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
+    code = np.where(pick_hi, hi, lo)
+    return (code | np.where(np.signbit(f), 0x80, 0)).astype(np.uint8)
+
+
+def quantize_tokens_fp8(x):
+    """Per-token FP8 (E4M3) quantization of the token rows.
+
+    ``scale[t] = max_c |x[t, c]| / 448`` and ``codes[t, c]`` the E4M3 code of
+    ``x[t, c] / scale[t]``, rounded to the nearest value, ties to even; a row
+    of zeros gets scale 0 and codes 0. The divisions run in float32, as for
+    the int8 codes (they decide the codes). Returns (codes uint8 [T, d],
+    scales float32 [T]).
+    """
+    xf = to_f64(x).astype(np.float32)
+    if xf.ndim != 2:
+        raise ValueError("x must be [T, d]")
+    absmax = np.abs(xf).max(axis=1) if xf.shape[1] else np.zeros(xf.shape[0], np.float32)
+    scales = (absmax / np.float32(E4M3_MAX)).astype(np.float32)
+    safe = np.where(scales > 0, scales, np.float32(1.0)).astype(np.float32)
+    codes = _e4m3_encode(xf / safe[:, None])  # float32 quotient, then exact rounding to E4M3
+    codes[scales == 0] = 0
+    return codes, scales
+
+
+def dequantize_tokens_fp8(codes, scales) -> np.ndarray:
+    """``value(codes[t, c]) * scales[t]`` in fp64 (the tokens GEMM1 sees)."""
+    return e4m3_values()[np.asarray(codes, dtype=np.int64)] * np.asarray(scales, dtype=np.float64)[:, None]
+
+
+def _dequantized(x, quant):
+    """The tokens the routed experts see under a token quantization."""
+    if quant == "int8":
+        return dequantize_tokens(*quantize_tokens(x))
+    if quant == "fp8":
+        return dequantize_tokens_fp8(*quantize_tokens_fp8(x))
+    return x
+
+
 # ---------------------------------------------------------------------------
 # expert parallelism, receive side (App. M: each GPU owns some experts; the
 # dispatch exchange brings it the rows of its own tokens and of its peer's
@@ -419,8 +496,9 @@ def layer(cfg: dict, x, w_router, bias, w_gate, w_up, w_down,
     cfg holds ``E, k, score, n_groups, topk_groups, renorm, scale`` and
     ``n_shared`` (0 or 1), and optionally ``quant`` ("int8": the routed
     experts see the tokens after :func:`quantize_tokens` and
-    :func:`dequantize_tokens`; the gate and the shared expert, which stay on
-    the sending side in the paper's pipeline, see the original tokens).
+    :func:`dequantize_tokens`; "fp8": after :func:`quantize_tokens_fp8` and
+    :func:`dequantize_tokens_fp8`; the gate and the shared expert, which stay
+    on the sending side in the paper's pipeline, see the original tokens).
     ``logits`` replaces the gate when given (used to re-route from logits
     computed elsewhere). The shared-expert weights are [I_s, d], [I_s, d] and
     [d, I_s]. Returns every intermediate.
@@ -430,7 +508,7 @@ def layer(cfg: dict, x, w_router, bias, w_gate, w_up, w_down,
     rb = None if cfg["score"] == "softmax" else bias
     topk_idx, topk_w, det = route(logits, bias=rb, return_detail=True, **_route_kwargs(cfg))
     counts, offsets, sorted_token, sorted_assign, inv_perm = dispatch(topk_idx, cfg["E"])
-    x_routed = dequantize_tokens(*quantize_tokens(x)) if cfg.get("quant") == "int8" else x
+    x_routed = _dequantized(x, cfg.get("quant"))
     y_perm = expert_ffn(x_routed, sorted_token, offsets, w_gate, w_up, w_down)
     shared = None
     if cfg.get("n_shared", 0):
@@ -451,13 +529,13 @@ def layer_rows(x, rows, topk_idx, topk_w, w_gate, w_up, w_down,
     ``out[t] = sum_j topk_w[t, j] * FFN_{topk_idx[t, j]}(x[t]) (+ shared(x[t]))``.
     rows: token indices; ``topk_idx``/``topk_w``: [len(rows), k] for those
     tokens. Experts are visited once each, so a large resident weight tensor
-    is decoded one expert at a time. ``quant="int8"``: the routed experts see
-    the quantized tokens (the quantization is per token, so a subset of rows
+    is decoded one expert at a time. ``quant="int8"`` or ``"fp8"``: the routed
+    experts see the quantized tokens (the quantization is per token, so a subset of rows
     quantizes as it would inside the whole batch). Returns [len(rows), d] in
     fp64.
     """
     X = to_f64(np.asarray(x)[np.asarray(rows, dtype=np.int64)])
-    Xr = dequantize_tokens(*quantize_tokens(np.asarray(x)[np.asarray(rows, dtype=np.int64)])) if quant == "int8" else X
+    Xr = _dequantized(np.asarray(x)[np.asarray(rows, dtype=np.int64)], quant) if quant in ("int8", "fp8") else X
     idx = np.asarray(topk_idx, dtype=np.int64)
     W = np.asarray(topk_w, dtype=np.float64)
     R, k = idx.shape

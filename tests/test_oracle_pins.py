@@ -626,3 +626,84 @@ def test_ep_receive_ffn_reduces_to_each_ranks_expert_ffn():
     xs2[:Tp] = xp
     bad = O.ep_receive_ffn(xs2, xp, rt, off, se, wg[e0:], wu[e0:], wd[e0:])
     assert not np.allclose(bad, y, rtol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# FP8 (OCP E4M3) token quantization
+# ---------------------------------------------------------------------------
+
+def test_fp8_worked_examples():
+    ex = json.load(open(os.path.join(GOLDEN, "fp8_examples.json")))
+    for name in ("F1", "F2", "F3"):
+        e = ex[name]
+        for x in (np.asarray([e["x"]], np.float32), _bf16_bits([e["x"]])):
+            codes, scales = O.quantize_tokens_fp8(x)
+            assert codes.dtype == np.uint8 and scales.dtype == np.float32
+            assert codes[0].tolist() == e["codes"], (name, codes[0].tolist())
+            assert float(scales[0]) == e["scale"], name
+
+
+def test_e4m3_code_table_properties():
+    v = O.e4m3_values()
+    nan = np.isnan(v)
+    assert nan.sum() == 2 and nan[0x7F] and nan[0xFF]
+    pos = v[:0x7F]
+    assert pos[0] == 0.0 and pos[0x7E] == 448.0 and v[0x38] == 1.0
+    assert (np.diff(pos) > 0).all()                       # codes order the values
+    np.testing.assert_array_equal(v[0x80:0xFF], -pos)    # the sign bit only negates
+    assert np.signbit(v[0x80])
+    # subnormals: 7 equal steps of 2^-9 up to the smallest normal 2^-6
+    np.testing.assert_array_equal(pos[:9], np.arange(9) * 2.0 ** -9)
+    # every binade [2^e, 2^(e+1)) of the normals holds 8 values 2^(e-3) apart (the top
+    # one 7: its eighth code is NaN)
+    for e in range(-6, 9):
+        b = pos[(pos >= 2.0 ** e) & (pos < 2.0 ** (e + 1))]
+        assert b.size == (7 if e == 8 else 8)
+        np.testing.assert_allclose(np.diff(b), 2.0 ** (e - 3))
+
+
+def test_fp8_quantize_invariants():
+    rng = np.random.default_rng(17)
+    x = (rng.standard_normal((48, 200)) * rng.uniform(0.01, 40, (48, 1))).astype(np.float32)
+    x[5] = 0.0
+    codes, scales = O.quantize_tokens_fp8(x)
+    v = O.e4m3_values()
+    assert not np.isnan(v[codes]).any()
+    nz = scales > 0
+    # the largest |x| of every non-zero row maps to +-448
+    assert (np.abs(v[codes[nz]]).max(axis=1) == 448.0).all()
+    assert scales[5] == 0 and (codes[5] == 0).all()
+    np.testing.assert_allclose(scales[nz], np.abs(x[nz]).max(axis=1) / 448.0, rtol=2 ** -23)
+    # round to nearest: within half a step of the grid at that magnitude (2^-4 relative for
+    # normals, 2^-10 absolute below the smallest normal), plus float32 rounding of the quotient
+    q = x[nz] / scales[nz, None]
+    err = np.abs(v[codes[nz]] - q)
+    step = np.where(np.abs(q) >= 2.0 ** -6, 2.0 ** (np.floor(np.log2(np.maximum(np.abs(q), 2.0 ** -6))) - 3), 2.0 ** -9)
+    assert (err <= step / 2 * (1 + 2 ** -20) + 1e-30).all()
+    # quantizing the grid values themselves changes nothing
+    c2, s2 = O.quantize_tokens_fp8(O.dequantize_tokens_fp8(codes, scales).astype(np.float32))
+    assert np.array_equal(c2[nz], codes[nz])
+    # per token: a subset of rows quantizes the same
+    c3, s3 = O.quantize_tokens_fp8(x[10:20])
+    assert np.array_equal(c3, codes[10:20]) and np.array_equal(s3, scales[10:20])
+
+
+def test_fp8_layer_equals_plain_layer_on_exact_tokens():
+    # tokens that are E4M3 values times a power of two, with max |x| = 448 times
+    # it, survive the quantization exactly, so the quantized layer is the plain one
+    rng = np.random.default_rng(13)
+    T, d, E, I = 16, 32, 4, 16
+    grid = O.e4m3_values()[:0x7F]
+    x = (rng.choice(grid, (T, d)) * rng.choice([-1.0, 1.0], (T, d)) * 0.125).astype(np.float32)
+    x[:, 0] = 448 * 0.125
+    wr = rng.standard_normal((E, d)) * 0.1
+    wg, wu = rng.standard_normal((E, I, d)) * 0.2, rng.standard_normal((E, I, d)) * 0.2
+    wd = rng.standard_normal((E, d, I)) * 0.2
+    cfg = dict(E=E, k=2, score="softmax", n_groups=1, topk_groups=1, renorm=True, scale=1.0, n_shared=0)
+    a = O.layer(cfg, x, wr, None, wg, wu, wd)
+    b = O.layer(dict(cfg, quant="fp8"), x, wr, None, wg, wu, wd)
+    assert np.array_equal(a["out"], b["out"])
+    x2 = x.copy()
+    x2[3, 5] = np.float32(1.03)   # between two grid values
+    assert not np.array_equal(O.layer(dict(cfg, quant="fp8"), x2, wr, None, wg, wu, wd)["out"],
+                              O.layer(cfg, x2, wr, None, wg, wu, wd)["out"])
