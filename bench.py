@@ -279,16 +279,12 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
     torch.cuda.synchronize()
     ffn_ms = f0.elapsed_time(f1) / steps
 
-    # int8 tokens (the pipeline's quantize-before-dispatch): the quantize
-    # kernel, the expert FFN on the codes and the layer with int8 tokens
-    q8 = None
+    # quantized tokens (the pipeline's quantize-before-dispatch, int8 and
+    # FP8): the quantize kernel, the expert FFN on the codes and the layer
+    # with quantized tokens
+    qres = {}
     if int8 and cfg.packed and not ffn_only:
         import dataclasses
-
-        codes = torch.empty((T, p["d"]), dtype=torch.int8, device="cuda")
-        scales = torch.empty(T, dtype=torch.float32, device="cuda")
-        cfg8 = dataclasses.replace(cfg, token_quant="int8")
-        ws8 = moe.alloc_workspace(cfg8, T)
 
         def timed(fn, n):
             for _ in range(max(2, warmup)):
@@ -302,20 +298,26 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
             torch.cuda.synchronize()
             return a.elapsed_time(b) / n
 
-        q_ms = timed(lambda: moe.moe_quantize(cfg, T, t["x"], codes, scales, stream=s_main), steps)
-        f8_ms = timed(lambda: moe.moe_expert_ffn_q8(cfg, T, codes, scales, dbg["sorted_token"], dbg["offsets"],
-                                                     w_ffn[0], w_ffn[2], y, ws, stream=s_main), steps)
-        l8_ms = timed(lambda: moe.moe_layer(cfg8, T, t["x"], t["w_router"], t["bias"], *w_ffn, *w_sh, out, ws8,
-                                            s_main=s_main, s_aux=s_aux), steps)
-        # token bytes the GEMM1 operand loads gather (every column tile reads its rows again)
-        nt1 = p["I"] // 128
-        rows = T * p["k"]
-        q8 = dict(quantize_ms=round(q_ms, 4), expert_ffn_ms=round(f8_ms, 4),
-                  expert_ffn_speedup=round(ffn_ms / f8_ms, 4), layer_ms=round(l8_ms, 4),
-                  tokens_per_s=round(T / (l8_ms / 1e3), 1),
-                  gathered_token_bytes_gemm1={"bf16": nt1 * rows * p["d"] * 2, "int8": nt1 * rows * p["d"]},
-                  note="layer with int8 tokens runs the shared expert outside the routed GEMMs")
-        del codes, scales, ws8
+        for mode in ("int8", "fp8"):
+            codes = torch.empty((T, p["d"]), dtype=torch.uint8, device="cuda")
+            scales = torch.empty(T, dtype=torch.float32, device="cuda")
+            cfgq = dataclasses.replace(cfg, token_quant=mode)
+            wsq = moe.alloc_workspace(cfgq, T)
+            q_ms = timed(lambda: moe.moe_quantize(cfgq, T, t["x"], codes, scales, stream=s_main), steps)
+            fq_ms = timed(lambda: moe.moe_expert_ffn_q8(cfgq, T, codes, scales, dbg["sorted_token"], dbg["offsets"],
+                                                         w_ffn[0], w_ffn[2], y, wsq, stream=s_main), steps)
+            lq_ms = timed(lambda: moe.moe_layer(cfgq, T, t["x"], t["w_router"], t["bias"], *w_ffn, *w_sh, out, wsq,
+                                                s_main=s_main, s_aux=s_aux), steps)
+            # token bytes the GEMM1 operand loads gather (every column tile reads its rows again)
+            nt1 = p["I"] // 128
+            rows = T * p["k"]
+            qres[mode] = dict(quantize_ms=round(q_ms, 4), expert_ffn_ms=round(fq_ms, 4),
+                              expert_ffn_speedup=round(ffn_ms / fq_ms, 4), layer_ms=round(lq_ms, 4),
+                              tokens_per_s=round(T / (lq_ms / 1e3), 1),
+                              gathered_token_bytes_gemm1={"bf16": nt1 * rows * p["d"] * 2,
+                                                          mode: nt1 * rows * p["d"]},
+                              note="layer with quantized tokens runs the shared expert outside the routed GEMMs")
+            del codes, scales, wsq
 
     ep_res = None
     if ep and cfg.packed and not ffn_only and p["E"] % 2 == 0 and p["dtype"] == "bf16":
@@ -323,7 +325,8 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
         ep_res = ep_split(p, t["x"], w_ffn[0], w_ffn[2], steps, warmup)
 
     res = dict(
-        name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms, int8_tokens=q8,
+        name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms,
+        int8_tokens=qres.get("int8"), fp8_tokens=qres.get("fp8"),
         ep_split=ep_res,
         counts_max_over_mean=float(counts.max() / counts.mean()), empty_experts=int((counts == 0).sum()),
         layer_hbm_frac=alg["layer_bytes"] / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
@@ -443,8 +446,9 @@ def main():
                                expert_ffn_roofline_frac=round(r["ffn_roof_frac"], 4),
                                touched_experts=r["alg"]["touched_experts"],
                                max_over_mean_load=round(r["counts_max_over_mean"], 3), empty_experts=r["empty_experts"])
-            if r["int8_tokens"]:
-                extra[name]["int8_tokens"] = r["int8_tokens"]
+            for key in ("int8_tokens", "fp8_tokens"):
+                if r[key]:
+                    extra[name][key] = r[key]
 
     r = main_res
     p = r["p"]
@@ -487,8 +491,9 @@ def main():
     }
     if "cpu" in r:
         out["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r["cpu"].items()}
-    if r["int8_tokens"]:
-        out["int8_tokens"] = r["int8_tokens"]
+    for key in ("int8_tokens", "fp8_tokens"):
+        if r[key]:
+            out[key] = r[key]
     if r["multilayer_ms_per_layer"]:
         out["multilayer"] = {"ms_per_layer": {str(L): round(v, 4) for L, v in r["multilayer_ms_per_layer"].items()},
                              "note": "L layer calls back to back on the same input and weights, each into its own output"}

@@ -88,9 +88,12 @@ typedef enum {
  * quantize before the dispatch exchange, dequantize before GEMM1). */
 typedef enum {
   MOE_QUANT_NONE = 0, /* the routed experts see the bf16/fp32 tokens                */
-  MOE_QUANT_INT8 = 1  /* int8 codes with one fp32 scale per token (moe_quantize);
+  MOE_QUANT_INT8 = 1, /* int8 codes with one fp32 scale per token (moe_quantize);
                          bf16 and MOE_LAYOUT_PACKED only; the gate and the shared
                          expert, on the sending side, keep the original tokens       */
+  MOE_QUANT_FP8 = 2   /* FP8 codes (OCP E4M3: 1 sign, 4 exponent bits with bias 7,
+                         3 mantissa bits; largest value 448, 0x7F/0xFF NaN) with one
+                         fp32 scale per token (Table 5's FP8 quantize); same rules   */
 } moe_quant_t;
 
 typedef struct {
@@ -187,13 +190,20 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x,
                    size_t ws_bytes, hipStream_t stream);
 
 /*
- * moe_quantize — per-token int8 quantization of the tokens (App. F pipeline,
- * the step before the dispatch exchange; App. M step (1)):
- *   scale[t]    = max_c |x[t][c]| / 127                       (fp32)
- *   codes[t][c] = x[t][c] / scale[t] in fp32, rounded half to even,
- *                 clamped to [-127, 127]; a zero row: scale 0, codes 0.
+ * moe_quantize — per-token quantization of the tokens (App. F pipeline,
+ * the step before the dispatch exchange; App. M step (1); Table 5's FP8
+ * quantize), selected by cfg->token_quant:
+ *  MOE_QUANT_FP8: scale[t]    = max_c |x[t][c]| / 448                 (fp32)
+ *                 codes[t][c] = E4M3 code of x[t][c] / scale[t], the fp32
+ *                               quotient clamped to [-448, 448] and rounded
+ *                               to the nearest value, ties to even;
+ *  otherwise int8: scale[t]    = max_c |x[t][c]| / 127                 (fp32)
+ *                 codes[t][c] = x[t][c] / scale[t] in fp32, rounded half to
+ *                               even, clamped to [-127, 127].
+ * A zero row: scale 0, codes 0 (code 0x80, E4M3 -0, marks a negative value
+ * that rounds to zero).
  *  x : [T][d] bf16 (cfg->dtype must be MOE_BF16).
- *  codes : [T][d] int8 out.   scales : [T] fp32 out.
+ *  codes : [T][d] bytes out (int8, or E4M3 bit patterns).   scales : [T] fp32 out.
  */
 int moe_quantize(const moe_config_t* cfg, int32_t T, const void* x, int8_t* codes, float* scales,
                  hipStream_t stream);
@@ -203,11 +213,12 @@ int moe_quantize(const moe_config_t* cfg, int32_t T, const void* x, int8_t* code
  * dequantize + GEMM1 + SwiGLU + GEMM2): for every expert e and row r,
  *   t = sorted_token[r], h[r] = silu(s_t q_t · w_gate[e]ᵀ) * (s_t q_t · w_up[e]ᵀ),
  *   y_perm[r] = h[r] · w_down[e]ᵀ
- * with q_t = codes[t], s_t = scales[t]. The dequantization is fused into
+ * with q_t the values of codes[t] (int8, or E4M3 when cfg->token_quant is
+ * MOE_QUANT_FP8) and s_t = scales[t]. The dequantization is fused into
  * GEMM1: the gathered code rows are converted to bf16 (exactly) as they are
  * loaded, and each row's sums are multiplied by its scale before the SwiGLU.
  * Packed weights only (cfg->weight_layout == MOE_LAYOUT_PACKED, bf16).
- *  codes : [T][d] int8, scales : [T] fp32 (from moe_quantize).
+ *  codes : [T][d] bytes, scales : [T] fp32 (from moe_quantize, same cfg).
  *  w_gate_up, w_down : packed weights from moe_pack_weights.
  *  y_perm : [T*k][d] bf16 out.
  */
@@ -252,7 +263,7 @@ int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const in
  *           it is computed inside the routed expert GEMMs as one more group
  *           (its compute fills the matrix cores of the memory-bound routed
  *           work); the result is the same.
- *           With cfg->token_quant == MOE_QUANT_INT8 the tokens are quantized
+ *           With cfg->token_quant MOE_QUANT_INT8 or MOE_QUANT_FP8 the tokens are quantized
  *           first (moe_quantize, into the workspace) and the routed experts
  *           run on the codes (moe_expert_ffn_q8); the gate and the shared
  *           expert use x, and the shared expert is then not fused.

@@ -91,7 +91,7 @@ Layout make_layout(const moe_config_t& c, int32_t T) {
   L.shared_h = take(c.n_shared ? t * c.I_shared * es : 0);
   L.shared_out = take(c.n_shared ? t * c.d * es : 0);
   L.queues = take(kQueueInts * 4);
-  const bool q8 = c.token_quant == MOE_QUANT_INT8;
+  const bool q8 = c.token_quant != MOE_QUANT_NONE;
   L.qcodes = take(q8 ? t * c.d : 0);  // moe_layer's quantized tokens
   L.qscales = take(q8 ? t * 4 : 0);
   L.total = off;
@@ -125,10 +125,10 @@ int validate(const moe_config_t* c, int32_t T) {
   if ((int64_t)T * c->k >= (int64_t)1 << 31) return fail(MOE_ERR_UNSUPPORTED, "T*k >= 2^31");
   if (c->weight_layout != MOE_LAYOUT_ROWMAJOR && c->weight_layout != MOE_LAYOUT_PACKED)
     return fail(MOE_ERR_INVALID_ARG, "unknown weight layout");
-  if (c->token_quant != MOE_QUANT_NONE && c->token_quant != MOE_QUANT_INT8)
+  if (c->token_quant != MOE_QUANT_NONE && c->token_quant != MOE_QUANT_INT8 && c->token_quant != MOE_QUANT_FP8)
     return fail(MOE_ERR_INVALID_ARG, "unknown token quantization");
-  if (c->token_quant == MOE_QUANT_INT8 && (c->dtype != MOE_BF16 || c->weight_layout != MOE_LAYOUT_PACKED))
-    return fail(MOE_ERR_UNSUPPORTED, "int8 tokens need bf16 and packed weights");
+  if (c->token_quant != MOE_QUANT_NONE && (c->dtype != MOE_BF16 || c->weight_layout != MOE_LAYOUT_PACKED))
+    return fail(MOE_ERR_UNSUPPORTED, "quantized tokens need bf16 and packed weights");
   if (c->weight_layout == MOE_LAYOUT_PACKED &&
       (c->dtype != MOE_BF16 || c->I % 128 != 0 || c->d % 256 != 0 || (c->n_shared && c->I_shared % 128 != 0)))
     return fail(MOE_ERR_UNSUPPORTED, "packed weights need bf16, I and I_shared % 128 == 0 and d % 256 == 0");
@@ -262,7 +262,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
                    int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
-                   int32_t max_wg = 0) {
+                   int32_t max_wg = 0, bool x_fp8 = false) {
   if (packed && queues) {
     const hipError_t e = moe::launch_queue_reset(queues, 16, s);
     if (e != hipSuccess) return e;
@@ -288,6 +288,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   }
   up.tile_queue = queues;
   up.a_scale = x_scales;
+  up.a_fp8 = x_fp8 ? 1 : 0;
   up.seg_end = seg_end;
   up.max_wg = max_wg;
   hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
@@ -511,13 +512,21 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
 
 int moe_quantize(const moe_config_t* cfg, int32_t T, const void* x, int8_t* codes, float* scales,
                  hipStream_t stream) {
-  MOE_CHECK(validate(cfg, T));
+  if (!cfg) return fail(MOE_ERR_INVALID_ARG, "config is NULL");
+  if (cfg->token_quant != MOE_QUANT_NONE && cfg->token_quant != MOE_QUANT_INT8 && cfg->token_quant != MOE_QUANT_FP8)
+    return fail(MOE_ERR_INVALID_ARG, "unknown token quantization");
+  // the quantization needs only the token shape: the weight rules do not apply
+  moe_config_t c = *cfg;
+  c.token_quant = MOE_QUANT_NONE;
+  c.weight_layout = MOE_LAYOUT_ROWMAJOR;
+  MOE_CHECK(validate(&c, T));
   if (cfg->dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "moe_quantize needs bf16 tokens");
   MOE_CHECK(need(x, "x"));
   MOE_CHECK(need(codes, "codes"));
   MOE_CHECK(need(scales, "scales"));
   if (T == 0) return MOE_OK;
-  const hipError_t e = moe::launch_quantize(x, codes, scales, T, cfg->d, stream);
+  const hipError_t e =
+      moe::launch_quantize(x, codes, scales, T, cfg->d, cfg->token_quant == MOE_QUANT_FP8, stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "quantize");
 }
 
@@ -539,8 +548,9 @@ int moe_expert_ffn_q8(const moe_config_t* cfg, int32_t T, const int8_t* codes, c
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, codes, sorted_token, offsets, w_gate_up, nullptr,
                                w_down, static_cast<char*>(ws) + L.h, y_perm, stream, true, nullptr,
-                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), scales);
-  return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN (int8 tokens)");
+                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), scales, nullptr, 0,
+                               cfg->token_quant == MOE_QUANT_FP8);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN (quantized tokens)");
 }
 
 int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void* ws_gate, const void* ws_up,
@@ -622,7 +632,8 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   // inside the routed expert GEMMs as one more group, so its compute fills
   // the matrix cores of the memory-bound routed work. Otherwise it runs on
   // its own, on s_aux when given (overlapping gate, routing and dispatch).
-  const bool q8 = c.token_quant == MOE_QUANT_INT8;
+  const bool q8 = c.token_quant != MOE_QUANT_NONE;  // int8 or FP8 codes
+  const bool f8 = c.token_quant == MOE_QUANT_FP8;
   const bool fuse = packed && c.n_shared && c.I_shared == c.I && !q8;
   const bool two = c.n_shared && !fuse && s_aux && s_aux != s_main;
   StreamEvents* ev = nullptr;
@@ -643,7 +654,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     return hip_fail(e, "dispatch");
   int8_t* const qcodes = reinterpret_cast<int8_t*>(w + L.qcodes);
   float* const qscales = reinterpret_cast<float*>(w + L.qscales);
-  if (q8 && (e = moe::launch_quantize(x, qcodes, qscales, T, c.d, s_main)) != hipSuccess)
+  if (q8 && (e = moe::launch_quantize(x, qcodes, qscales, T, c.d, f8, s_main)) != hipSuccess)
     return hip_fail(e, "quantize");
   FusedShared fs;
   if (fuse) {
@@ -653,7 +664,8 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     fs.out = shared;
   }
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
-                   w_down, w + L.h, y, s_main, packed, fuse ? &fs : nullptr, queues, q8 ? qscales : nullptr)) !=
+                   w_down, w + L.h, y, s_main, packed, fuse ? &fs : nullptr, queues, q8 ? qscales : nullptr, nullptr,
+                   0, f8)) !=
       hipSuccess)
     return hip_fail(e, "expert FFN");
   if (c.n_shared && !fuse) {

@@ -1,4 +1,6 @@
 // Weight-streaming grouped bf16 GEMM over packed expert weights (gfx950).
+// (GEMM1 also takes its token rows as per-token-scaled int8 or FP8 codes,
+// converted to bf16 exactly while staged into LDS.)
 //
 // The expert FFN of the MoE layer (App. M step 3; App. F GEMM1 + SwiGLU +
 // GEMM2) at DeepSeek-V3 shape is bound by reading every expert's weights
@@ -99,6 +101,22 @@ __device__ __forceinline__ void codes_to_bf16(i32x4 v, i32x4& lo, i32x4& hi) {
   hi = i32x4{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
 }
 
+// 16 FP8 codes (OCP E4M3, element e in byte e) -> the same 16 values as
+// bf16. Every E4M3 value (3 mantissa bits, exponents 2^-9 .. 2^8) is exact
+// in bf16, so keeping the high half of the converted fp32 value is exact.
+__device__ __forceinline__ void fp8_to_bf16(i32x4 v, i32x4& lo, i32x4& hi) {
+  uint32_t o[8];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const auto f01 = __builtin_amdgcn_cvt_pk_f32_fp8(v[d], false);  // bytes 0, 1
+    const auto f23 = __builtin_amdgcn_cvt_pk_f32_fp8(v[d], true);   // bytes 2, 3
+    o[2 * d] = __builtin_amdgcn_perm(__float_as_uint(f01[1]), __float_as_uint(f01[0]), 0x07060302u);
+    o[2 * d + 1] = __builtin_amdgcn_perm(__float_as_uint(f23[1]), __float_as_uint(f23[0]), 0x07060302u);
+  }
+  lo = i32x4{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+  hi = i32x4{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+}
+
 template <typename F, int... Is>
 __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
   (f(std::integral_constant<int, Is>{}), ...);
@@ -141,7 +159,7 @@ __device__ __forceinline__ int scan4(int v, int* scratch, int* total) {
 
 // EPI_SWIGLU: GEMM1 (j = gate/up, 32 output columns per wave);
 // EPI_STORE:  GEMM2 (j = two 32-column halves, 64 output columns per wave).
-template <int EPI, bool Q8>
+template <int EPI, bool Q8, bool F8 = false>
 __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
   constexpr int WCOLS = (EPI == EPI_SWIGLU) ? 32 : 64;  // output columns per wave
   constexpr int TCOLS = WCOLS * kWaves;                  // per tile
@@ -199,7 +217,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   // + 0..7): lane l carries row l/8 of the block and the logical 16-byte chunk
   // that lds_off() places at physical chunk l%8.
   const int lr = lane >> 3, lc = (lane & 7) ^ ((wave * 4 + (lr >> 1)) & 7);
-  // Q8: A rows of int8 codes move in 1 KB blocks of 16 rows of 64 bytes
+  // Q8: A rows of 1-byte codes (int8, or FP8 with F8) move in 1 KB blocks of 16 rows of 64 bytes
   // (block i of a wave: rows 64 i + 16 wave + 0..15): lane l carries row l/4
   // and codes 16 (l%4) .. 16 (l%4) + 15 of the step's 64.
   const int lr8 = lane >> 2, lc8 = lane & 3;
@@ -329,7 +347,8 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
           for (int i = 0; i < A_CH; ++i) {
             const int r = i * 16 * kWaves + wave * 16 + lr8;
             i32x4 lo, hi;
-            codes_to_bf16(sa[decltype(s_c)::value][i], lo, hi);
+            if constexpr (F8) fp8_to_bf16(sa[decltype(s_c)::value][i], lo, hi);
+            else codes_to_bf16(sa[decltype(s_c)::value][i], lo, hi);
             *reinterpret_cast<i32x4*>(slot + lds_off(r, 2 * lc8)) = lo;
             *reinterpret_cast<i32x4*>(slot + lds_off(r, 2 * lc8 + 1)) = hi;
           }
@@ -563,9 +582,9 @@ __global__ void pack_kernel(const __bf16* __restrict__ w0, const __bf16* __restr
   }
 }
 
-template <int EPI, bool Q8>
+template <int EPI, bool Q8, bool F8 = false>
 hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
-  auto kern = gemm_stream_kernel<EPI, Q8>;
+  auto kern = gemm_stream_kernel<EPI, Q8, F8>;
   // the A ring, reused after each tile's K loop as the LDS copy of its output
   constexpr size_t lds = std::max<size_t>((size_t)kSlots * kMaxRows * 128,
                                           (size_t)kMaxRows * ((EPI == EPI_SWIGLU) ? 128 : 256) * 2);
@@ -598,7 +617,10 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
 
 hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
   if ((p.M <= 0 && p.x_rows <= 0) || p.N <= 0) return hipSuccess;
-  if (p.a_scale) return epi == EPI_SWIGLU ? launch_stream<EPI_SWIGLU, true>(p, s) : hipErrorInvalidValue;
+  if (p.a_scale) {
+    if (epi != EPI_SWIGLU) return hipErrorInvalidValue;
+    return p.a_fp8 ? launch_stream<EPI_SWIGLU, true, true>(p, s) : launch_stream<EPI_SWIGLU, true>(p, s);
+  }
   if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU, false>(p, s);
   return launch_stream<EPI_STORE, false>(p, s);
 }

@@ -63,11 +63,13 @@ struct GemmProblem {
   // launch, from which workgroups claim tiles after their first (nullptr:
   // a static round-robin schedule).
   int32_t* tile_queue;
-  // Weight-streaming kernel, EPI_SWIGLU only: A holds int8 codes ([*][K]
-  // bytes) of rows whose fp32 scales are a_scale[A row]; every output row's
+  // Weight-streaming kernel, EPI_SWIGLU only: A holds int8 (or, with a_fp8,
+  // E4M3) codes ([*][K] bytes) of rows whose fp32 scales are a_scale[A row]; every output row's
   // gate and up sums are multiplied by its row's scale before the SwiGLU.
   // The extra group must be empty (x_rows == 0). nullptr: A is bf16.
   const float* a_scale;
+  // With a_scale: the codes are FP8 (OCP E4M3) values instead of int8.
+  int32_t a_fp8;
   // Weight-streaming kernel only: group g owns rows [offsets[g], seg_end[g])
   // instead of [offsets[g], offsets[g+1]) (nullptr: adjacent segments), so a
   // call can cover part of every group's rows.
@@ -134,10 +136,12 @@ struct CombineParams {
 };
 hipError_t launch_combine(const CombineParams& p, bool bf16, hipStream_t s);
 
-// Per-token int8 quantization: codes[t][c] = rne(x[t][c] / scale[t]) clamped
-// to +-127, scale[t] = max_c |x[t][c]| / 127 (0 and codes 0 for a zero row).
-// x bf16 [T][d], d % 64 == 0; codes int8 [T][d]; scales fp32 [T].
-hipError_t launch_quantize(const void* x, int8_t* codes, float* scales, int T, int d, hipStream_t s);
+// Per-token quantization. int8: codes[t][c] = rne(x[t][c] / scale[t])
+// clamped to +-127, scale[t] = max_c |x[t][c]| / 127; fp8: E4M3 codes of
+// x[t][c] / scale[t] (clamped to +-448, round to nearest even), scale[t] =
+// max_c |x[t][c]| / 448. A zero row: scale 0, codes 0. x bf16 [T][d],
+// d % 64 == 0; codes [T][d] bytes; scales fp32 [T].
+hipError_t launch_quantize(const void* x, int8_t* codes, float* scales, int T, int d, bool fp8, hipStream_t s);
 
 // Receive side of expert parallelism: fills the self (mode 0) or remote
 // (mode 1) rows of experts [e0, e1) of a receive buffer whose expert e owns

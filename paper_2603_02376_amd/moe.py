@@ -22,7 +22,8 @@ LIB_PATH = os.path.join(_PKG, "libmoe.so")
 MOE_F32, MOE_BF16 = 0, 1
 MOE_SCORE_SOFTMAX, MOE_SCORE_SIGMOID = 0, 1
 MOE_LAYOUT_ROWMAJOR, MOE_LAYOUT_PACKED = 0, 1
-MOE_QUANT_NONE, MOE_QUANT_INT8 = 0, 1
+MOE_QUANT_NONE, MOE_QUANT_INT8, MOE_QUANT_FP8 = 0, 1, 2
+_QUANT = {"none": MOE_QUANT_NONE, "int8": MOE_QUANT_INT8, "fp8": MOE_QUANT_FP8}
 MOE_EP_SELF, MOE_EP_REMOTE = 0, 1
 EP_SCHEDULES = {"sequential": 0, "self_remote": 1, "expert_chunks": 2}
 STATUS = {0: "MOE_OK", -1: "MOE_ERR_INVALID_ARG", -2: "MOE_ERR_UNSUPPORTED",
@@ -122,7 +123,7 @@ class MoeConfig:
     scale: float = 1.0
     dtype: str = "bf16"        # "bf16" | "f32"
     weight_layout: str = "rowmajor"  # "rowmajor" | "packed" (expert weights, see moe_pack_weights)
-    token_quant: str = "none"        # "none" | "int8" (tokens the routed experts receive)
+    token_quant: str = "none"        # "none" | "int8" | "fp8" (tokens the routed experts receive)
 
     @property
     def torch_dtype(self):
@@ -134,7 +135,7 @@ class MoeConfig:
                             int(bool(self.renorm)), float(self.scale),
                             MOE_BF16 if self.dtype == "bf16" else MOE_F32,
                             MOE_LAYOUT_PACKED if self.weight_layout == "packed" else MOE_LAYOUT_ROWMAJOR,
-                            MOE_QUANT_INT8 if self.token_quant == "int8" else MOE_QUANT_NONE)
+                            _QUANT[self.token_quant])
 
     @property
     def packed(self) -> bool:
@@ -226,21 +227,29 @@ def moe_expert_ffn(cfg: MoeConfig, T, x, sorted_token, offsets, w_gate, w_up, w_
                                 _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def _codes(codes, n):
+    """Codes buffer: 1-byte elements (int8, uint8 or float8_e4m3fn storage)."""
+    if codes is not None and codes.element_size() != 1:
+        raise TypeError(f"codes must have 1-byte elements, got {codes.dtype}")
+    return _ptr(codes, "codes", None, n)
+
+
 def moe_quantize(cfg: MoeConfig, T, x, codes, scales, stream=None):
-    """Per-token int8 quantization: codes int8 [T, d], scales fp32 [T]."""
+    """Per-token quantization (cfg.token_quant "fp8": E4M3 codes, else int8):
+    codes [T, d] (1-byte elements), scales fp32 [T]."""
     c = cfg.c()
-    _check(lib().moe_quantize(ctypes.byref(c), T, _ptr(x, "x", cfg.torch_dtype, T * cfg.d),
-                              _ptr(codes, "codes", torch.int8, T * cfg.d), _ptr(scales, "scales", torch.float32, T),
-                              _stream(stream)))
+    _check(lib().moe_quantize(ctypes.byref(c), T, _ptr(x, "x", cfg.torch_dtype, T * cfg.d), _codes(codes, T * cfg.d),
+                              _ptr(scales, "scales", torch.float32, T), _stream(stream)))
 
 
 def moe_expert_ffn_q8(cfg: MoeConfig, T, codes, scales, sorted_token, offsets, w_gate_up, w_down, y_perm, ws,
                       stream=None):
-    """Expert FFN on int8 tokens (packed weights from :func:`pack_weights`)."""
+    """Expert FFN on quantized tokens (codes from :func:`moe_quantize` with the
+    same cfg; packed weights from :func:`pack_weights`)."""
     c = cfg.c()
     n = T * cfg.k
     wsz = cfg.E * cfg.I * cfg.d
-    _check(lib().moe_expert_ffn_q8(ctypes.byref(c), T, _ptr(codes, "codes", torch.int8, T * cfg.d),
+    _check(lib().moe_expert_ffn_q8(ctypes.byref(c), T, _codes(codes, T * cfg.d),
                                    _ptr(scales, "scales", torch.float32, T),
                                    _ptr(sorted_token, "sorted_token", torch.int32, n),
                                    _ptr(offsets, "offsets", torch.int32, cfg.E + 1),

@@ -1,10 +1,11 @@
-"""GPU parity of the int8 token path (App. F pipeline: quantize the tokens
-before the dispatch exchange, dequantize them before GEMM1), through the C ABI.
+"""GPU parity of the quantized token paths (App. F pipeline: quantize the
+tokens before the dispatch exchange, dequantize them before GEMM1; int8, and
+FP8 (OCP E4M3) as Table 5 names), through the C ABI.
 
-moe_quantize: codes and scales bit-exact against the oracle (integers decided
-in fp32 on both sides). moe_expert_ffn_q8 and moe_layer with int8 tokens: the
-oracle's FFN on the dequantized tokens, within the bf16 tolerance; integer
-results of the layer bit-exact.
+moe_quantize: codes and scales bit-exact against the oracle (codes decided in
+fp32 on both sides). moe_expert_ffn_q8 and moe_layer with quantized tokens:
+the oracle's FFN on the dequantized tokens, within the bf16 tolerance;
+integer results of the layer bit-exact.
 """
 import numpy as np
 import pytest
@@ -27,23 +28,41 @@ def _bf16(a):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16).cuda()
 
 
+def _oracle_quant(mode):
+    return (O.quantize_tokens, O.dequantize_tokens) if mode == "int8" else (O.quantize_tokens_fp8,
+                                                                            O.dequantize_tokens_fp8)
+
+
+def _codes_buf(mode, T, d):
+    return torch.empty((T, d), dtype=torch.int8 if mode == "int8" else torch.uint8, device="cuda")
+
+
+@pytest.mark.parametrize("mode", ["int8", "fp8"])
 @pytest.mark.parametrize("T,d", [(1, 64), (37, 256), (300, 7168), (4096, 7168)])
-def test_quantize_bit_exact(T, d):
-    log("quantize", T, d)
+def test_quantize_bit_exact(T, d, mode):
+    log("quantize", mode, T, d)
     rng = np.random.default_rng(T + d)
     x = (rng.standard_normal((T, d)) * rng.uniform(0.05, 20, (T, 1))).astype(np.float32)
     if T > 2:
         x[1] = 0.0                                    # zero row: scale 0, codes 0
-        # a row of exact halves: max |x| = 127 * 2^-3, scale 2^-3, codes = x * 8 with .5 ties
-        x[2] = (rng.integers(-254, 255, d) * 0.0625).astype(np.float32)
-        x[2, 0] = 127 * 0.125
+        if mode == "int8":
+            # a row of exact halves: max |x| = 127 * 2^-3, scale 2^-3, codes = x * 8 with .5 ties
+            x[2] = (rng.integers(-254, 255, d) * 0.0625).astype(np.float32)
+            x[2, 0] = 127 * 0.125
+        else:
+            # a row of E4M3 grid values and midpoints between neighbours (ties), max |x| = 448:
+            # scale 1, every tie rule and the subnormals exercised
+            g = O.e4m3_values()[:0x7F]
+            pts = np.concatenate([g, (g[1:] + g[:-1]) / 2])
+            x[2] = (rng.choice(pts, d) * rng.choice([-1.0, 1.0], d)).astype(np.float32)
+            x[2, 0] = 448.0
     xb = _bf16(x)
-    cfg = moe.MoeConfig(d=d, E=8, k=2, I=128, dtype="bf16")
-    codes = torch.empty((T, d), dtype=torch.int8, device="cuda")
+    cfg = moe.MoeConfig(d=d, E=8, k=2, I=128, dtype="bf16", weight_layout="packed", token_quant=mode)
+    codes = _codes_buf(mode, T, d)
     scales = torch.empty(T, dtype=torch.float32, device="cuda")
     moe.moe_quantize(cfg, T, xb, codes, scales)
     torch.cuda.synchronize()
-    want_c, want_s = O.quantize_tokens(inputs.oracle_view(xb))
+    want_c, want_s = _oracle_quant(mode)[0](inputs.oracle_view(xb))
     assert np.array_equal(host(scales), want_s)
     got_c = host(codes)
     if not np.array_equal(got_c, want_c):
@@ -70,24 +89,26 @@ def _topk(T, E, k, rng, hot):
     return idx
 
 
+@pytest.mark.parametrize("mode", ["int8", "fp8"])
 @pytest.mark.parametrize("case", QCASES, ids=lambda c: "T{}_d{}_E{}_k{}_I{}".format(*c[:5]))
-def test_expert_ffn_q8(case):
+def test_expert_ffn_q8(case, mode):
     T, d, E, k, I, hot = case
-    log("expert_ffn_q8", case)
+    log("expert_ffn_q8", mode, case)
     p = dict(T=T, d=d, E=E, k=k, I=I, dtype="bf16", n_shared=0, bias="none")
     t = inputs.make_inputs(p, 0, "cuda")
     idx = _topk(T, E, k, np.random.default_rng(T), hot)
     counts, offsets, st, sa, inv = O.dispatch(idx, E)
-    cfg = moe.MoeConfig(d=d, E=E, k=k, I=I, dtype="bf16", weight_layout="packed")
+    cfg = moe.MoeConfig(d=d, E=E, k=k, I=I, dtype="bf16", weight_layout="packed", token_quant=mode)
     gu, dn = moe.pack_weights(cfg, t["w_gate"], t["w_up"], t["w_down"])
-    codes = torch.empty((T, d), dtype=torch.int8, device="cuda")
+    codes = _codes_buf(mode, T, d)
     scales = torch.empty(T, dtype=torch.float32, device="cuda")
     moe.moe_quantize(cfg, T, t["x"], codes, scales)
     ws = moe.alloc_workspace(cfg, T)
     y = torch.full((T * k, d), float("nan"), dtype=torch.bfloat16, device="cuda")
     moe.moe_expert_ffn_q8(cfg, T, codes, scales, _dev(st), _dev(offsets), gu, dn, y, ws)
     torch.cuda.synchronize()
-    xq = O.dequantize_tokens(host(codes), host(scales))
+    quant, dequant = _oracle_quant(mode)
+    xq = dequant(host(codes), host(scales))
     want = O.expert_ffn(xq, st, offsets, inputs.ExpertView(t["w_gate"]), inputs.ExpertView(t["w_up"]),
                         inputs.ExpertView(t["w_down"]))
     got = host(y.float())
@@ -96,7 +117,7 @@ def test_expert_ffn_q8(case):
     log("  max_rel_err", err)
     assert err <= BF16_TOL
     # the codes fed to the GEMM are the oracle's codes
-    wc, ws_ = O.quantize_tokens(inputs.oracle_view(t["x"]))
+    wc, ws_ = quant(inputs.oracle_view(t["x"]))
     assert np.array_equal(host(codes), wc) and np.array_equal(host(scales), ws_)
 
 
@@ -112,9 +133,10 @@ def test_expert_ffn_q8_rejects_unpacked_and_f32():
     with pytest.raises(moe.MoeError) as e:
         moe.moe_expert_ffn_q8(cfg, 4, z8, zs, zi, offsets, zw, zw, y, ws)
     assert e.value.status == -2
-    with pytest.raises(moe.MoeError) as e:   # int8 tokens in the layer need packed weights too
-        moe.alloc_workspace(moe.MoeConfig(d=256, E=8, k=2, I=128, dtype="bf16", token_quant="int8"), 4)
-    assert e.value.status in (-1, -2)
+    for mode in ("int8", "fp8"):   # quantized tokens in the layer need packed weights too
+        with pytest.raises(moe.MoeError) as e:
+            moe.alloc_workspace(moe.MoeConfig(d=256, E=8, k=2, I=128, dtype="bf16", token_quant=mode), 4)
+        assert e.value.status in (-1, -2)
 
 
 LAYER_CASES = {
@@ -125,16 +147,18 @@ LAYER_CASES = {
 }
 
 
+@pytest.mark.parametrize("mode", ["int8", "fp8"])
 @pytest.mark.parametrize("name", list(LAYER_CASES))
-def test_layer_int8_tokens(name):
-    p = dict(LAYER_CASES[name], weight_layout="packed", token_quant="int8")
-    log("layer int8 tokens", name)
+def test_layer_quantized_tokens(name, mode):
+    p = dict(LAYER_CASES[name], weight_layout="packed", token_quant=mode)
+    log("layer quantized tokens", mode, name)
     t = G.device_inputs(p, seed=3)
     r = G.run_layer(p, t)
     G.check_logits(p, t, r)
     routing = G.check_routing_and_dispatch_exact(p, t, r)
     x = inputs.oracle_view(t["x"])
-    xq = O.dequantize_tokens(*O.quantize_tokens(x))
+    quant, dequant = _oracle_quant(mode)
+    xq = dequant(*quant(x))
     y = O.expert_ffn(xq, host(r["sorted_token"]), host(r["offsets"]), inputs.ExpertView(t["w_gate"]),
                      inputs.ExpertView(t["w_up"]), inputs.ExpertView(t["w_down"]))
     sh = None
@@ -152,9 +176,10 @@ def test_layer_int8_tokens(name):
     assert torch.equal(r2["out"], r["out"])
 
 
-def test_layer_int8_tokens_full_size_sampled():
-    p = dict(inputs.preset("dsv3"), weight_layout="packed", token_quant="int8")
-    log("full-size layer, int8 tokens")
+@pytest.mark.parametrize("mode", ["int8", "fp8"])
+def test_layer_quantized_tokens_full_size_sampled(mode):
+    p = dict(inputs.preset("dsv3"), weight_layout="packed", token_quant=mode)
+    log("full-size layer, quantized tokens", mode)
     t = G.device_inputs(p, seed=0, cache_weights=True)
     r = G.run_layer(p, t)
     G.check_logits(p, t, r)
@@ -163,7 +188,7 @@ def test_layer_int8_tokens_full_size_sampled():
     rows = np.unique(np.concatenate([[0, p["T"] - 1], rng.choice(p["T"], 8, replace=False)]))
     want = O.layer_rows(inputs.oracle_view(t["x"]), rows, routing["topk_idx"][rows], routing["topk_w"][rows],
                         inputs.ExpertView(t["w_gate"]), inputs.ExpertView(t["w_up"]), inputs.ExpertView(t["w_down"]),
-                        *(inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")), quant="int8")
+                        *(inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")), quant=mode)
     err = max_rel_err(host(r["out"].float())[rows], want)
     log("  sampled out max_rel_err", err)
     assert err <= BF16_TOL
