@@ -225,7 +225,8 @@ hipError_t run_gate_route(const moe_config_t& c, int32_t T, const void* x, const
 }
 
 hipError_t run_dispatch(const moe_config_t& c, int32_t T, const int32_t* idx, char* ws, const Layout& L,
-                        int32_t* counts, int32_t* offsets, int32_t* st, int32_t* sa, int32_t* inv, hipStream_t s) {
+                        int32_t* counts, int32_t* offsets, int32_t* st, int32_t* sa, int32_t* inv, hipStream_t s,
+                        int32_t* zero = nullptr, int32_t n_zero = 0) {
   moe::DispatchParams d{};
   d.topk_idx = idx;
   d.T = T;
@@ -238,6 +239,8 @@ hipError_t run_dispatch(const moe_config_t& c, int32_t T, const int32_t* idx, ch
   d.sorted_token = st;
   d.sorted_assign = sa;
   d.inv_perm = inv;
+  d.zero = zero;
+  d.n_zero = n_zero;
   return moe::launch_dispatch(d, s);
 }
 
@@ -254,7 +257,8 @@ struct FusedShared {
 // y = h Wdᵀ into `y`. packed: weights from moe_pack_weights (wu unused) and
 // the weight-streaming kernel; fused (packed only, same intermediate size):
 // the shared expert over all a_rows tokens rides along as an extra group.
-// queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path.
+// queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path, zeroed
+// here unless queues_zeroed (moe_layer zeroes them in its dispatch).
 // x_scales: x holds int8 codes of rows with these fp32 scales (packed only).
 // seg_end, max_wg (packed only): group g owns rows [offsets[g], seg_end[g]);
 // at most max_wg workgroups per GEMM (0: one per compute unit).
@@ -262,8 +266,8 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
                    int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
-                   int32_t max_wg = 0, bool x_fp8 = false) {
-  if (packed && queues) {
+                   int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false) {
+  if (packed && queues && !queues_zeroed) {
     const hipError_t e = moe::launch_queue_reset(queues, 16, s);
     if (e != hipSuccess) return e;
   }
@@ -650,7 +654,9 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   if ((e = run_gate_route(c, T, x, w_router, bias, logits, reinterpret_cast<float*>(w + L.gate_partials), idx, tw,
                           s_main)) != hipSuccess)
     return hip_fail(e, "route");
-  if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main)) != hipSuccess)
+  // the dispatch also zeroes the routed FFN's 16 tile-queue heads (packed weights)
+  if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main, packed ? queues : nullptr,
+                        packed ? 16 : 0)) != hipSuccess)
     return hip_fail(e, "dispatch");
   int8_t* const qcodes = reinterpret_cast<int8_t*>(w + L.qcodes);
   float* const qscales = reinterpret_cast<float*>(w + L.qscales);
@@ -665,7 +671,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   }
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
                    w_down, w + L.h, y, s_main, packed, fuse ? &fs : nullptr, queues, q8 ? qscales : nullptr, nullptr,
-                   0, f8)) !=
+                   0, f8, /*queues_zeroed=*/true)) !=
       hipSuccess)
     return hip_fail(e, "expert FFN");
   if (c.n_shared && !fuse) {

@@ -14,7 +14,8 @@
 //   2. scan    — one workgroup: per expert, the exclusive prefix of popcounts
 //                over chunks (the chunk's base inside the expert's segment),
 //                the per-expert count, and the exclusive prefix over experts
-//                (offsets).
+//                (offsets); optionally it also zeroes the expert GEMMs'
+//                tile-queue heads.
 //   3. scatter — same grid as 1: the row of (t, j) is
 //                offsets[e] + base[chunk][e] + popcount(mask[chunk][e] & lanes below t),
 //                i.e. the number of earlier tokens that chose e.
@@ -52,6 +53,7 @@ __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
   __shared__ int wsum[16];
   const int e = threadIdx.x & 255;
   const int part = threadIdx.x >> 8;
+  if (p.zero && (int)threadIdx.x < p.n_zero) p.zero[threadIdx.x] = 0;
   const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;
   const int per = (nchunks + 3) / 4;
   const int c0 = part * per, c1 = min(nchunks, c0 + per);

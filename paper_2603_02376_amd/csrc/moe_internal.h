@@ -123,6 +123,10 @@ struct DispatchParams {
   int32_t* sorted_token;
   int32_t* sorted_assign;  // may be nullptr
   int32_t* inv_perm;
+  // Optional: n_zero ints at `zero` (the expert GEMMs' tile-queue heads) set
+  // to 0 by the scan kernel, saving a launch before the expert FFN.
+  int32_t* zero;
+  int32_t n_zero;
 };
 hipError_t launch_dispatch(const DispatchParams& p, hipStream_t s);
 

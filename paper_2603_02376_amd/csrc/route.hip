@@ -14,8 +14,9 @@
 // deterministic function of the fp32 logits' bits and a near-tie in fp32
 // cannot flip it. Group scores (sum of a group's two largest keys) come from
 // a per-wave LDS copy of the keys; the best groups and then the k best
-// experts are found by k rounds of a wave-wide butterfly argmax on
-// (key descending, index ascending).
+// experts are found by rounds of a wave-wide argmax on (key descending,
+// index ascending), built from DPP lane exchanges within 16-lane rows and
+// reads of the four row results.
 #include "moe_internal.h"
 
 namespace moe {
@@ -32,29 +33,84 @@ __device__ __forceinline__ bool better(double ka, int ia, double kb, int ib) {
   return ka > kb || (ka == kb && ia < ib);
 }
 
+// Wave-wide reductions. Four DPP steps combine the lanes of each 16-lane row
+// (swap neighbours, swap pairs, mirror within 8 lanes, mirror within 16);
+// the four row results are then read as wave-uniform values (lanes 0, 16,
+// 32, 48) and combined in a fixed order, so every lane gets the same result.
+// Every call is made with all 64 lanes active.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)dpp_i32<CTRL>((int)(uint32_t)b);
+  const uint32_t hi = (uint32_t)dpp_i32<CTRL>((int)(uint32_t)(b >> 32));
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+template <int CTRL>
+__device__ __forceinline__ void argmax_step(double& key, int& idx) {
+  const double ok = dpp_f64<CTRL>(key);
+  const int oi = dpp_i32<CTRL>(idx);
+  if (better(ok, oi, key, idx)) {
+    key = ok;
+    idx = oi;
+  }
+}
+
 __device__ __forceinline__ KeyIdx wave_argmax(double key, int idx) {
+  argmax_step<kDppXor1>(key, idx);
+  argmax_step<kDppXor2>(key, idx);
+  argmax_step<kDppHalfMirror>(key, idx);
+  argmax_step<kDppMirror>(key, idx);
+  KeyIdx b{readlane_f64(key, 0), __builtin_amdgcn_readlane(idx, 0)};
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const double ok = __shfl_xor(key, o, 64);
-    const int oi = __shfl_xor(idx, o, 64);
-    if (better(ok, oi, key, idx)) {
-      key = ok;
-      idx = oi;
+  for (int r = 1; r < 4; ++r) {
+    const double k = readlane_f64(key, 16 * r);
+    const int i = __builtin_amdgcn_readlane(idx, 16 * r);
+    if (better(k, i, b.key, b.idx)) {
+      b.key = k;
+      b.idx = i;
     }
   }
-  return {key, idx};
+  return b;
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_f64<kDppXor1>(v);
+  v += dpp_f64<kDppXor2>(v);
+  v += dpp_f64<kDppHalfMirror>(v);
+  v += dpp_f64<kDppMirror>(v);
+  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
 __device__ __forceinline__ double wave_max(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmax(v, dpp_f64<kDppXor1>(v));
+  v = fmax(v, dpp_f64<kDppXor2>(v));
+  v = fmax(v, dpp_f64<kDppHalfMirror>(v));
+  v = fmax(v, dpp_f64<kDppMirror>(v));
+  return fmax(fmax(readlane_f64(v, 0), readlane_f64(v, 16)), fmax(readlane_f64(v, 32), readlane_f64(v, 48)));
+}
+
+// Top two (as a multiset) of the keys held by a run of lanes: each lane
+// starts with the top two of its own keys (m1 >= m2) and merges with a
+// partner lane's pair at every step.
+template <int CTRL>
+__device__ __forceinline__ void top2_step(double& m1, double& m2) {
+  const double b1 = dpp_f64<CTRL>(m1), b2 = dpp_f64<CTRL>(m2);
+  const double n2 = (m1 >= b1) ? fmax(m2, b1) : fmax(m1, b2);
+  m1 = fmax(m1, b1);
+  m2 = n2;
 }
 
 template <int EPL>
@@ -68,16 +124,19 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
 
   // ---- scores and keys ---------------------------------------------------
   double key[EPL], score[EPL];
-  float u[EPL];
+  float u[EPL], bv[EPL];
   // Logits: the K-split partials summed in ascending split order. Each
   // round issues the loads of up to 8 splits for all of the lane's experts
   // before adding them, so the loads overlap instead of waiting one by one.
+  // The selection bias is loaded with them (not inside the score loop, where
+  // every load would be waited for on its own).
   {
     constexpr int R = 8;
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
       const int e = lane * EPL + i;
       u[i] = (active && e < E) ? p.logits_in[(size_t)t * E + e] : 0.f;
+      bv[i] = (p.bias && e < E) ? p.bias[e] : 0.f;
     }
     for (int sp0 = 1; sp0 < p.nsplit; sp0 += R) {
       float part[R][EPL];
@@ -107,7 +166,7 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
       score[i] = 0.0;
     } else if (p.score == 1) {  // sigmoid
       score[i] = 1.0 / (1.0 + exp(-(double)u[i]));
-      key[i] = score[i] + (p.bias ? (double)p.bias[e] : 0.0);
+      key[i] = score[i] + (double)bv[i];
     } else {  // softmax: select on the logit; probabilities come later
       score[i] = (double)u[i];
       key[i] = (double)u[i];
@@ -118,12 +177,45 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
   bool elig[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) elig[i] = (lane * EPL + i) < E;
-  if (p.n_groups > 1) {
+  const int gs = p.n_groups > 1 ? E / p.n_groups : E;  // experts per group
+  const int lpg = gs / EPL;                             // lanes per group when gs % EPL == 0
+  if (p.n_groups > 1 && E == 64 * EPL && gs % EPL == 0 && (lpg == 2 || lpg == 4 || lpg == 8 || lpg == 16)) {
+    // Every group is a run of lpg lanes. Its score (sum of its two largest
+    // keys) comes from merging the lanes' top-two pairs within the run; the
+    // groups are then ranked on the wave-uniform scores read from the first
+    // lane of each run (score descending, index ascending), and a group is
+    // kept when fewer than topk_groups groups rank above it.
+    double m1 = NEG, m2 = NEG;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const double v = key[i];
+      if (v > m1) {
+        m2 = m1;
+        m1 = v;
+      } else if (v > m2) {
+        m2 = v;
+      }
+    }
+    top2_step<kDppXor1>(m1, m2);
+    if (lpg >= 4) top2_step<kDppXor2>(m1, m2);
+    if (lpg >= 8) top2_step<kDppHalfMirror>(m1, m2);
+    if (lpg >= 16) top2_step<kDppMirror>(m1, m2);
+    const double gscore = m1 + m2;
+    const int g = lane / lpg;
+    int rank = 0;
+    for (int h = 0; h < p.n_groups; ++h) {
+      const double o = readlane_f64(gscore, h * lpg);
+      if (better(o, h, gscore, g)) ++rank;
+    }
+    if (rank >= p.topk_groups) {
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) elig[i] = false;
+    }
+  } else if (p.n_groups > 1) {
 #pragma unroll
     for (int i = 0; i < EPL; ++i)
       if (lane * EPL + i < E) skeys[wave][lane * EPL + i] = key[i];
     __syncthreads();
-    const int gs = E / p.n_groups;
     double gscore = NEG;
     if (lane < p.n_groups) {
       double m1 = NEG, m2 = NEG;
@@ -170,14 +262,15 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
       }
     }
     const KeyIdx w = wave_argmax(bk, bi);
-    double sc = 0.0;
+    // the winner's score, read from the lane that holds it (w is wave-uniform)
+    const int wl = (w.idx / EPL) & 63, wi = w.idx % EPL;
+    double own = score[0];
 #pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if (lane * EPL + i == w.idx) {
-        taken[i] = true;
-        sc = score[i];
-      }
-    sc = wave_sum(sc);  // exactly one lane holds the winner's score
+    for (int i = 0; i < EPL; ++i) {
+      if (i == wi) own = score[i];
+      if (lane * EPL + i == w.idx) taken[i] = true;
+    }
+    const double sc = readlane_f64(own, wl);
     if (lane == j) {
       my_e = w.idx;
       my_score = sc;
