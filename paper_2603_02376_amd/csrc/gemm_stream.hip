@@ -72,6 +72,23 @@ constexpr int kUnroll = 6;         // K-loop unroll: a multiple of kDepth, kSlot
 constexpr int kStreamStore = 19;   // cache policy of output stores: sc0 sc1 nt (streaming, not kept in L2)
 static_assert(kUnroll % kDepth == 0 && kUnroll % kSlots == 0 && kUnroll % kStage == 0, "unroll");
 
+template <bool DEEP>
+struct StreamCfg {
+  static constexpr int rows = kMaxRows, depth = kDepth, slots = kSlots, unroll = kUnroll;
+};
+template <>
+struct StreamCfg<true> {
+  static constexpr int rows = 160, depth = 4, slots = 4, unroll = 4;
+};
+// Pipeline shapes. The default one keeps two weight steps in flight and
+// takes passes of up to 192 rows; the deep one keeps three in flight, which
+// fits the register file with passes of up to 160 rows. Deep is measured
+// faster for GEMM2 when the groups are small (DeepSeek-V3 shape, ~128 rows
+// per expert: many short tiles) and for GEMM1 when the shared expert rides
+// along as an extra group of full passes; groups of many passes (the
+// Mixtral shape, hot experts) prefer the larger passes.
+constexpr int kDeepMaxAvgRows = 160;
+
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
@@ -159,8 +176,11 @@ __device__ __forceinline__ int scan4(int v, int* scratch, int* total) {
 
 // EPI_SWIGLU: GEMM1 (j = gate/up, 32 output columns per wave);
 // EPI_STORE:  GEMM2 (j = two 32-column halves, 64 output columns per wave).
-template <int EPI, bool Q8, bool F8 = false>
+template <int EPI, bool Q8, bool F8, bool DEEP>
 __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
+  constexpr int kMaxRows = StreamCfg<DEEP>::rows, kDepth = StreamCfg<DEEP>::depth;
+  constexpr int kSlots = StreamCfg<DEEP>::slots, kUnroll = StreamCfg<DEEP>::unroll;
+  static_assert(kUnroll % kDepth == 0 && kUnroll % kSlots == 0 && kUnroll % kStage == 0, "unroll");
   constexpr int WCOLS = (EPI == EPI_SWIGLU) ? 32 : 64;  // output columns per wave
   constexpr int TCOLS = WCOLS * kWaves;                  // per tile
   // Dynamic LDS: the A ring (kSlots slots of kMaxRows x 128 bytes).
@@ -582,10 +602,11 @@ __global__ void pack_kernel(const __bf16* __restrict__ w0, const __bf16* __restr
   }
 }
 
-template <int EPI, bool Q8, bool F8 = false>
+template <int EPI, bool Q8, bool F8 = false, bool DEEP = false>
 hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
-  auto kern = gemm_stream_kernel<EPI, Q8, F8>;
+  auto kern = gemm_stream_kernel<EPI, Q8, F8, DEEP>;
   // the A ring, reused after each tile's K loop as the LDS copy of its output
+  constexpr int kMaxRows = StreamCfg<DEEP>::rows, kSlots = StreamCfg<DEEP>::slots;
   constexpr size_t lds = std::max<size_t>((size_t)kSlots * kMaxRows * 128,
                                           (size_t)kMaxRows * ((EPI == EPI_SWIGLU) ? 128 : 256) * 2);
   static std::once_flag once;
@@ -621,7 +642,13 @@ hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
     if (epi != EPI_SWIGLU) return hipErrorInvalidValue;
     return p.a_fp8 ? launch_stream<EPI_SWIGLU, true, true>(p, s) : launch_stream<EPI_SWIGLU, true>(p, s);
   }
-  if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU, false>(p, s);
+  const int groups = p.offsets ? p.groups : 1;
+  const bool small = groups > 0 && (long long)p.M <= (long long)kDeepMaxAvgRows * groups;
+  if (epi == EPI_SWIGLU) {
+    if (small && p.x_rows > 0) return launch_stream<EPI_SWIGLU, false, false, true>(p, s);
+    return launch_stream<EPI_SWIGLU, false>(p, s);
+  }
+  if (small) return launch_stream<EPI_STORE, false, false, true>(p, s);
   return launch_stream<EPI_STORE, false>(p, s);
 }
 
