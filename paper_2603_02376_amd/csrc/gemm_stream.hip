@@ -143,13 +143,15 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-template <int N, typename F>
-__device__ __forceinline__ void with_count(int n, F&& f) {
-  if constexpr (N == 0) {
-    f(std::integral_constant<int, 0>{});
+// Calls f(std::integral_constant<int, n>) for a runtime n in [LO, N] (n < LO
+// runs the LO instance).
+template <int N, int LO, typename F>
+__device__ __forceinline__ void with_count_from(int n, F&& f) {
+  if constexpr (N <= LO) {
+    f(std::integral_constant<int, LO>{});
   } else {
     if (n == N) f(std::integral_constant<int, N>{});
-    else with_count<N - 1>(n, f);
+    else with_count_from<N - 1, LO>(n, f);
   }
 }
 
@@ -265,6 +267,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     int a_rows, row0, rows, nt;
     const char* b_base;
     __bf16* c_base;
+    bool multi;  // the tile's group takes more than one pass
     if (extra) {
       a_base = p.xA;
       a_rows = p.x_rows;
@@ -272,6 +275,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       nt = seg;
       row0 = (off - r_len) * kMaxRows;
       rows = min(kMaxRows, p.x_rows - row0);
+      multi = units_x > 1;
       b_base = static_cast<const char*>(p.xB) + (size_t)nt * nk * kWaves * kStepBytes;
       c_base = static_cast<__bf16*>(p.xC);
     } else {
@@ -287,6 +291,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       const int local = rt - tstart[e] * Nt;
       const int passes = tstart[e + 1] - tstart[e];
       const int pass = local % passes;
+      multi = passes > 1;
       nt = local / passes;
       const int gbeg = p.offsets ? min(max(p.offsets[e], 0), p.M) : 0;
       const int gend = p.offsets ? min(max(p.seg_end ? p.seg_end[e] : p.offsets[e + 1], gbeg), p.M) : p.M;
@@ -313,8 +318,13 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     const int nact = __builtin_amdgcn_readfirstlane((rows + 31) / 32);
 
-    auto body = [&](auto ar_c) __attribute__((always_inline)) {
+    // TEMPORAL: weight loads that stay in L2 (a full pass of a group that
+    // takes several passes: the group's other passes of the same column tile
+    // run next to it and find its weights there); otherwise non-temporal
+    // loads (weights read once).
+    auto body = [&](auto ar_c, auto temporal_c) __attribute__((always_inline)) {
       constexpr int AR = decltype(ar_c)::value;  // A rows staged per step (128 or kMaxRows)
+      constexpr bool TEMPORAL = decltype(temporal_c)::value;
       constexpr int A_CH = Q8 ? AR / (16 * kWaves) : AR / (8 * kWaves);  // A loads per wave per step
       constexpr int LOADS = A_CH + 8;
       uint32_t a_off[A_CH];  // byte offsets into A (its size is checked below 4 GiB at launch)
@@ -354,8 +364,9 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       };
       auto load_b = [&](int ks, auto s_c, int n) __attribute__((always_inline)) {
         const int kc = min(ks, nk - 1);
-        bq[decltype(s_c)::value][n] = __builtin_nontemporal_load(
-            reinterpret_cast<const i32x4*>(bw + (size_t)kc * kWaves * kStepBytes + n * 1024));
+        const i32x4* const src = reinterpret_cast<const i32x4*>(bw + (size_t)kc * kWaves * kStepBytes + n * 1024);
+        if constexpr (TEMPORAL) bq[decltype(s_c)::value][n] = *src;
+        else bq[decltype(s_c)::value][n] = __builtin_nontemporal_load(src);
       };
       // Write A register set S into ring slot R (layout of lds_off(): lane l
       // holds row l/8 of each 8-row block, at physical chunk l%8). Q8: each
@@ -479,10 +490,12 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
           if (ks + u_c < nk) step(ks + u_c, std::integral_constant<int, decltype(u_c)::value % kUnroll>{}, std::true_type{});
         });
       };
-      with_count<AR / 32>(min(nact, AR / 32), kloop);
+      // a pass of more than 128 rows has at least 5 fragments
+      with_count_from<AR / 32, (AR > 128 ? 5 : 0)>(min(nact, AR / 32), kloop);
     };
-    if (rows <= 128) body(std::integral_constant<int, 128>{});
-    else body(std::integral_constant<int, kMaxRows>{});
+    if (rows <= 128) body(std::integral_constant<int, 128>{}, std::false_type{});
+    else if (multi) body(std::integral_constant<int, kMaxRows>{}, std::true_type{});
+    else body(std::integral_constant<int, kMaxRows>{}, std::false_type{});
 
     // ---- epilogue. The MFMAs take the weights as their first operand, so
     // acc[i][j] is the transposed 32x32 tile: lane l holds token row

@@ -283,6 +283,8 @@ PACKED_CASES = [
     (64, 256, 64, 8, 128, None),       # ~8 rows per expert, some experts empty
     (700, 256, 4, 2, 128, None),       # 350 rows per expert: 192 + 158
     (513, 768, 32, 8, 384, None),
+    (320, 256, 4, 2, 128, None),       # 160 rows per expert on average: deep pipeline (160-row passes)
+    (322, 256, 4, 2, 128, None),       # 161 on average: default pipeline (192-row passes)
 ]
 
 
