@@ -221,6 +221,16 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   const int total_tiles = routed_tiles + Nt * units_x;
   auto seg_start = [&](int j) { return (int)((int64_t)j * routed_tiles / Nt) + j * units_x; };
   const int nk = p.K / 64;
+  // Rows [row0, row0 + rows) of pass `pass` of a group of c rows taking
+  // `passes` passes: the group's 32-row fragments are spread evenly over its
+  // passes (at most kMaxRows / 32 each), so the passes of one column tile take
+  // about the same time and stay together, sharing the tile's weights in L2.
+  auto pass_rows = [&](int c, int passes, int pass, int& row0, int& rows) __attribute__((always_inline)) {
+    const int nfrag = (c + 31) / 32;
+    const int base = nfrag / passes, rem = nfrag % passes;
+    row0 = 32 * (pass * base + min(pass, rem));
+    rows = min(32 * (base + (pass < rem ? 1 : 0)), c - row0);
+  };
   const int G = gridDim.x, b = blockIdx.x;
   // Schedule. Workgroups are dealt to the 8 XCDs round-robin (b % 8); XCD x
   // owns the queue of tiles {r G + x W + j : j < W} (W = G / 8, r = 0, 1,
@@ -273,8 +283,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       a_rows = p.x_rows;
       gather = nullptr;
       nt = seg;
-      row0 = (off - r_len) * kMaxRows;
-      rows = min(kMaxRows, p.x_rows - row0);
+      pass_rows(p.x_rows, units_x, off - r_len, row0, rows);
       multi = units_x > 1;
       b_base = static_cast<const char*>(p.xB) + (size_t)nt * nk * kWaves * kStepBytes;
       c_base = static_cast<__bf16*>(p.xC);
@@ -298,8 +307,8 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       a_base = p.A;
       a_rows = p.a_rows;
       gather = p.gather;
-      row0 = gbeg + pass * kMaxRows;
-      rows = min(kMaxRows, gend - row0);
+      pass_rows(gend - gbeg, passes, pass, row0, rows);
+      row0 += gbeg;
       b_base = static_cast<const char*>(p.B0) + ((size_t)e * Nt + nt) * nk * kWaves * kStepBytes;
       c_base = static_cast<__bf16*>(p.C);
     }
