@@ -327,10 +327,10 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     const int nact = __builtin_amdgcn_readfirstlane((rows + 31) / 32);
 
-    // TEMPORAL: weight loads that stay in L2 (a full pass of a group that
-    // takes several passes: the group's other passes of the same column tile
-    // run next to it and find its weights there); otherwise non-temporal
-    // loads (weights read once).
+    // TEMPORAL: weight loads that stay in L2 (a pass of a group that takes
+    // several passes: the group's other passes of the same column tile run
+    // next to it and find its weights there); otherwise non-temporal loads
+    // (weights read once).
     auto body = [&](auto ar_c, auto temporal_c) __attribute__((always_inline)) {
       constexpr int AR = decltype(ar_c)::value;  // A rows staged per step (128 or kMaxRows)
       constexpr bool TEMPORAL = decltype(temporal_c)::value;
@@ -499,11 +499,15 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
           if (ks + u_c < nk) step(ks + u_c, std::integral_constant<int, decltype(u_c)::value % kUnroll>{}, std::true_type{});
         });
       };
-      // a pass of more than 128 rows has at least 5 fragments
-      with_count_from<AR / 32, (AR > 128 ? 5 : 0)>(min(nact, AR / 32), kloop);
+      // A pass of more than 128 rows has at least 5 fragments; with the
+      // fragments spread evenly, every pass of a group that takes several
+      // passes has at least 3.
+      with_count_from<AR / 32, (AR > 128 ? 5 : (TEMPORAL ? 3 : 0))>(min(nact, AR / 32), kloop);
     };
-    if (rows <= 128) body(std::integral_constant<int, 128>{}, std::false_type{});
-    else if (multi) body(std::integral_constant<int, kMaxRows>{}, std::true_type{});
+    if (rows <= 128) {
+      if (multi) body(std::integral_constant<int, 128>{}, std::true_type{});
+      else body(std::integral_constant<int, 128>{}, std::false_type{});
+    } else if (multi) body(std::integral_constant<int, kMaxRows>{}, std::true_type{});
     else body(std::integral_constant<int, kMaxRows>{}, std::false_type{});
 
     // ---- epilogue. The MFMAs take the weights as their first operand, so
