@@ -15,8 +15,11 @@
 //     output columns.
 //   * Weights for kDepth-1 steps ahead stay in flight per wave (a ring of
 //     register sets, the K loop unrolled so every set is statically indexed).
+//     Two pipeline shapes: default (two steps in flight, passes of up to 192
+//     rows) and deep (three steps in flight, passes of up to 160 rows), the
+//     launcher choosing one from the average rows per group.
 //   * The token rows (A, gathered through sorted_token) are shared by the 4
-//     waves through a three-slot LDS ring: each wave loads its share of a
+//     waves through an LDS ring of three or four slots: each wave loads its share of a
 //     step's rows into registers three steps ahead and writes them to the
 //     ring two steps ahead; one barrier per step publishes them. The first
 //     K slice of the next step is read before that barrier, so neither the
@@ -29,12 +32,14 @@
 //     the LDS reads of the next 16-wide K slice and an even share of the
 //     step's loads, so a load waiting for queue space never idles the matrix
 //     core for long.
-//   * A pass covers up to 192 rows of one expert (the accumulators of 6 row
-//     fragments x 2 column fragments live in AGPRs, one wave per SIMD), so
-//     every uniformly routed DeepSeek-V3 expert (128 +- 11 rows) is one pass
-//     and its weights are read exactly once; longer segments take more
-//     passes, which are ordered side by side so they share the weight stream
-//     through L2.
+//   * A pass covers up to 192 (160) rows of one expert (the accumulators of
+//     6 (5) row fragments x 2 column fragments live in AGPRs, one wave per
+//     SIMD), so every uniformly routed DeepSeek-V3 expert (128 +- 11 rows) is
+//     one pass and its weights are read exactly once, with non-temporal
+//     loads. Longer segments take more passes: their fragments are spread
+//     evenly over the passes, the passes of one column tile are ordered side
+//     by side, and their weight loads are cached, so the passes run together
+//     and share the weight stream through L2.
 //   * The K loop is compiled per count of active 32-row fragments, so the
 //     MFMA stream has no branches.
 //   * The MFMAs take the weights as their first operand and the token rows
