@@ -319,6 +319,65 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
                               note="layer with quantized tokens runs the shared expert outside the routed GEMMs")
             del codes, scales, wsq
 
+    # where the shared expert runs: inside the routed GEMMs (moe_layer with
+    # packed weights), or as its own FFN composed from the public calls, on
+    # the routing stream after the routed FFN, or on a second stream forked
+    # before the router GEMM (the paper's two-stream overlap: it runs beside
+    # routing, dispatch and the routed FFN; the combine waits for it)
+    sh_res = None
+    if ep and cfg.packed and p["n_shared"] and not ffn_only:
+        log(f"[bench] {name}: shared expert fused vs composed on one or two streams")
+        E, k = p["E"], p["k"]
+        i32 = dict(dtype=torch.int32, device="cuda")
+        b = dict(logits=torch.empty((T, E), dtype=torch.float32, device="cuda"),
+                 idx=torch.empty((T, k), **i32), w=torch.empty((T, k), dtype=torch.float32, device="cuda"),
+                 counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32), st=torch.empty(T * k, **i32),
+                 inv=torch.empty(T * k, **i32), y=torch.empty((T * k, p["d"]), dtype=cfg.torch_dtype, device="cuda"),
+                 sh=torch.empty((T, p["d"]), dtype=cfg.torch_dtype, device="cuda"), out=torch.empty_like(out))
+        fork, join = torch.cuda.Event(), torch.cuda.Event()
+
+        def shared(stream):
+            moe.moe_shared_ffn(cfg, T, t["x"], *w_sh, b["sh"], ws, stream=stream)
+
+        def composed(two):
+            if two:
+                fork.record(s_main)
+                s_aux.wait_event(fork)
+                shared(s_aux)
+                join.record(s_aux)
+            moe.moe_route(cfg, T, t["x"], t["w_router"], t["bias"], b["logits"], b["idx"], b["w"], ws, stream=s_main)
+            moe.moe_dispatch(cfg, T, b["idx"], b["counts"], b["offsets"], b["st"], None, b["inv"], ws, stream=s_main)
+            moe.moe_expert_ffn(cfg, T, t["x"], b["st"], b["offsets"], *w_ffn, b["y"], ws, stream=s_main)
+            if two:
+                s_main.wait_event(join)
+            else:
+                shared(s_main)
+            moe.moe_combine(cfg, T, b["y"], b["inv"], b["w"], b["sh"], b["out"], stream=s_main)
+
+        def timed_main(fn):
+            for _ in range(max(2, warmup)):
+                fn()
+            torch.cuda.synchronize()
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s_main)
+            for _ in range(steps):
+                fn()
+            z.record(s_main)
+            torch.cuda.synchronize()
+            return a.elapsed_time(z) / steps
+
+        one_ms = timed_main(lambda: composed(False))
+        two_ms = timed_main(lambda: composed(True))
+        sh_ms = timed_main(lambda: shared(s_main))
+        layer()
+        torch.cuda.synchronize()
+        sh_res = dict(fused_layer_ms=round(ms, 4), composed_one_stream_ms=round(one_ms, 4),
+                      composed_two_streams_ms=round(two_ms, 4), shared_ffn_alone_ms=round(sh_ms, 4),
+                      routed_ffn_alone_ms=round(ffn_ms, 4), outputs_identical=bool(torch.equal(out, b["out"])),
+                      note="composed: moe_route, moe_dispatch, moe_expert_ffn, moe_shared_ffn and moe_combine; "
+                           "two streams: the shared FFN on a second stream from the start, joined before the combine")
+        del b
+
     ep_res = None
     if ep and cfg.packed and not ffn_only and p["E"] % 2 == 0 and p["dtype"] == "bf16":
         log(f"[bench] {name}: expert-parallel receive side, ratios {inputs.EP_RATIOS}")
@@ -327,7 +386,7 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
     res = dict(
         name=name, p=p, ms=ms, wall_s=wall, tokens_per_s=T / (ms / 1e3), alg=alg, ffn_ms=ffn_ms,
         int8_tokens=qres.get("int8"), fp8_tokens=qres.get("fp8"),
-        ep_split=ep_res,
+        ep_split=ep_res, shared_expert=sh_res,
         counts_max_over_mean=float(counts.max() / counts.mean()), empty_experts=int((counts == 0).sum()),
         layer_hbm_frac=alg["layer_bytes"] / (ms / 1e3) / (HBM_PEAK_GBS * 1e9),
         layer_mfma_frac=alg["layer_flops"] / (ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12),
@@ -497,6 +556,8 @@ def main():
     if r["multilayer_ms_per_layer"]:
         out["multilayer"] = {"ms_per_layer": {str(L): round(v, 4) for L, v in r["multilayer_ms_per_layer"].items()},
                              "note": "L layer calls back to back on the same input and weights, each into its own output"}
+    if r["shared_expert"]:
+        out["shared_expert"] = r["shared_expert"]
     if r["ep_split"]:
         out["ep_split"] = r["ep_split"]
     if extra:
