@@ -16,8 +16,8 @@
 //   * Weights for kDepth-1 steps ahead stay in flight per wave (a ring of
 //     register sets, the K loop unrolled so every set is statically indexed).
 //     Two pipeline shapes: default (two steps in flight, passes of up to 192
-//     rows) and deep (three steps in flight, passes of up to 160 rows), the
-//     launcher choosing one from the average rows per group.
+//     rows) and deep (three steps in flight, passes of up to 160 rows, for
+//     GEMM2 over small groups).
 //   * The token rows (A, gathered through sorted_token) are shared by the 4
 //     waves through an LDS ring of three or four slots: each wave loads its share of a
 //     step's rows into registers three steps ahead and writes them to the
@@ -88,10 +88,9 @@ struct StreamCfg<true> {
 // Pipeline shapes. The default one keeps two weight steps in flight and
 // takes passes of up to 192 rows; the deep one keeps three in flight, which
 // fits the register file with passes of up to 160 rows. Deep is measured
-// faster for GEMM2 when the groups are small (DeepSeek-V3 shape, ~128 rows
-// per expert: many short tiles) and for GEMM1 when the shared expert rides
-// along as an extra group of full passes; groups of many passes (the
-// Mixtral shape, hot experts) prefer the larger passes.
+// faster for GEMM2 (K = I: short tiles) when the groups are small
+// (DeepSeek-V3 shape, ~128 rows per expert); GEMM1 and groups of many
+// passes (the Mixtral shape) prefer the default.
 constexpr int kDeepMaxAvgRows = 160;
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -675,10 +674,7 @@ hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
   }
   const int groups = p.offsets ? p.groups : 1;
   const bool small = groups > 0 && (long long)p.M <= (long long)kDeepMaxAvgRows * groups;
-  if (epi == EPI_SWIGLU) {
-    if (small && p.x_rows > 0) return launch_stream<EPI_SWIGLU, false, false, true>(p, s);
-    return launch_stream<EPI_SWIGLU, false>(p, s);
-  }
+  if (epi == EPI_SWIGLU) return launch_stream<EPI_SWIGLU, false>(p, s);
   if (small) return launch_stream<EPI_STORE, false, false, true>(p, s);
   return launch_stream<EPI_STORE, false>(p, s);
 }
