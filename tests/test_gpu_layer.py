@@ -17,7 +17,7 @@ import torch
 
 from oracle import moe_oracle as O
 from oracle.checks import max_rel_err
-from paper_2603_02376_amd import inputs
+from paper_2603_02376_amd import inputs, moe
 from tests import gpu_util as G
 
 pytestmark = pytest.mark.gpu
@@ -109,6 +109,45 @@ def test_layer_on_side_streams():
     with torch.cuda.stream(s1):
         r = G.run_layer(p, t, s_main=s1, s_aux=s2)
     assert torch.equal(ref["out"], r["out"])
+
+
+@pytest.mark.parametrize("two_streams", [False, True])
+def test_layer_fused_shared_equals_composed_calls(two_streams):
+    # moe_layer with packed weights runs the shared expert inside the routed
+    # GEMMs; composing the layer from the public calls (route, dispatch, routed
+    # FFN, shared FFN on the same or a second stream, combine) must give the
+    # same bits: every output element is summed in the same order.
+    p = dict(SMALL["dsv3_like_bf16"], d=512, I=256, I_shared=256, weight_layout="packed")
+    t = G.device_inputs(p, seed=6)
+    ref = G.run_layer(p, t)
+    cfg = G.moe_cfg(p)
+    T, k, E, d = p["T"], p["k"], p["E"], p["d"]
+    gu, dn = moe.pack_weights(cfg, t["w_gate"], t["w_up"], t["w_down"])
+    sg, sd = moe.pack_shared_weights(cfg, t["ws_gate"], t["ws_up"], t["ws_down"])
+    ws = moe.alloc_workspace(cfg, T)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    logits = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    idx, w = torch.empty((T, k), **i32), torch.empty((T, k), dtype=torch.float32, device="cuda")
+    counts, offsets = torch.empty(E, **i32), torch.empty(E + 1, **i32)
+    st, inv = torch.empty(T * k, **i32), torch.empty(T * k, **i32)
+    y = torch.empty((T * k, d), dtype=torch.bfloat16, device="cuda")
+    sh, out = (torch.empty((T, d), dtype=torch.bfloat16, device="cuda") for _ in range(2))
+    s_main = torch.cuda.current_stream()
+    s_aux = torch.cuda.Stream() if two_streams else s_main
+    fork, join = torch.cuda.Event(), torch.cuda.Event()
+    fork.record(s_main)
+    s_aux.wait_event(fork)
+    moe.moe_shared_ffn(cfg, T, t["x"], sg, None, sd, sh, ws, stream=s_aux)
+    join.record(s_aux)
+    moe.moe_route(cfg, T, t["x"], t["w_router"], t["bias"], logits, idx, w, ws, stream=s_main)
+    moe.moe_dispatch(cfg, T, idx, counts, offsets, st, None, inv, ws, stream=s_main)
+    moe.moe_expert_ffn(cfg, T, t["x"], st, offsets, gu, None, dn, y, ws, stream=s_main)
+    s_main.wait_event(join)
+    moe.moe_combine(cfg, T, y, inv, w, sh, out, stream=s_main)
+    torch.cuda.synchronize()
+    assert torch.equal(ref["shared_out"], sh)
+    assert torch.equal(ref["y_perm"], y)
+    assert torch.equal(ref["out"], out)
 
 
 # ---------------------------------------------------------------------------
