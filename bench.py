@@ -13,7 +13,9 @@ the plain [E][I][d] weights instead. Prints ONE JSON line: tokens/s of the
 layer, the roofline of the dominant kernel pair (the grouped expert FFN,
 timed with HIP events on its own stream), the CPU oracle timed on a bounded
 sample of the same workload as a baseline, the per-layer time of 1, 4 and 16
-layer calls run back to back, the receive side of two-GPU expert parallelism
+layer calls run back to back, the layer with the shared expert inside the
+routed GEMMs against the same layer composed from the public calls with the
+shared expert on one or two streams, the receive side of two-GPU expert parallelism
 under the three schedules of moe_ep_expert_ffn for imbalance ratios 2:1 to
 5:1 (the exchange emulated by a copy with a fixed workgroup budget), and side
 measurements of the skewed-routing, decode-sized and Mixtral-shaped
