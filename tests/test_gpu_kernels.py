@@ -36,6 +36,11 @@ ROUTE_CASES = [
     (1000, 256, 8, 8, 4, "sigmoid", True, True, 2.5),
     (4096, 256, 8, 8, 4, "sigmoid", False, True, 2.5),
     (129, 96, 5, 4, 2, "sigmoid", True, False, 1.5),
+    # groups as runs of 2, 4 and 16 lanes (E = 256: 4 experts per lane), and of 8 lanes at E = 128
+    (300, 256, 8, 32, 8, "sigmoid", True, True, 2.5),
+    (300, 256, 8, 16, 6, "sigmoid", True, True, 2.5),
+    (300, 256, 8, 4, 2, "sigmoid", True, True, 2.5),
+    (200, 128, 6, 8, 3, "softmax", False, True, 1.0),
     (64, 12, 4, 3, 2, "sigmoid", True, True, 1.0),
     (33, 256, 16, 1, 1, "sigmoid", True, True, 2.5),
     (50, 4, 4, 1, 1, "softmax", False, True, 1.0),       # k = E
