@@ -14,7 +14,7 @@
 namespace moe {
 namespace {
 
-constexpr int kThreads = 128;
+constexpr int kThreads = 64;
 constexpr int kMaxK = 16;
 
 struct Vec8 {
