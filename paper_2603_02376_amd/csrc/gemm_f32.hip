@@ -26,8 +26,6 @@ __device__ __forceinline__ int group_of_row(const int32_t* offsets, int groups, 
 template <int EPI>
 __global__ void __launch_bounds__(TS * TS) gemm_f32_kernel(GemmProblem p) {
   __shared__ float as[TS][KS + 1];
-  __shared__ float b0s[TS][KS + 1];
-  __shared__ float b1s[TS][KS + 1];
   const int tx = threadIdx.x % TS, ty = threadIdx.x / TS;
   const int row_base = blockIdx.y * TS;
   const int col_base = blockIdx.x * TS;
