@@ -318,7 +318,7 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
                               tokens_per_s=round(T / (lq_ms / 1e3), 1),
                               gathered_token_bytes_gemm1={"bf16": nt1 * rows * p["d"] * 2,
                                                           mode: nt1 * rows * p["d"]},
-                              note="layer with quantized tokens runs the shared expert outside the routed GEMMs")
+                              note="layer with quantized tokens runs the shared expert's GEMM1 on its own (bf16 input) and its GEMM2 inside the routed GEMM2")
             del codes, scales, wsq
 
     # where the shared expert runs: inside the routed GEMMs (moe_layer with

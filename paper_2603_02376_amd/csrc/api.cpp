@@ -245,7 +245,9 @@ hipError_t run_dispatch(const moe_config_t& c, int32_t T, const int32_t* idx, ch
 }
 
 // The shared expert fused into the routed weight-streaming launches as one
-// extra group: its packed weights, its intermediate and output buffers.
+// extra group: its packed weights, its intermediate and output buffers
+// (w_gate_up == nullptr: its GEMM1 has run on its own and only GEMM2 takes
+// it along).
 struct FusedShared {
   const void* w_gate_up = nullptr;
   const void* w_down = nullptr;
@@ -284,7 +286,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   up.K = c.d;
   up.C = h;
   up.ldc = inter;
-  if (fused) {
+  if (fused && fused->w_gate_up) {
     up.xA = x;
     up.xB = fused->w_gate_up;
     up.xC = fused->h;
@@ -639,7 +641,11 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   const bool q8 = c.token_quant != MOE_QUANT_NONE;  // int8 or FP8 codes
   const bool f8 = c.token_quant == MOE_QUANT_FP8;
   const bool fuse = packed && c.n_shared && c.I_shared == c.I && !q8;
-  const bool two = c.n_shared && !fuse && s_aux && s_aux != s_main;
+  // With quantized tokens the shared expert's GEMM1 (bf16 input) runs on its
+  // own before the routed GEMM1, and its GEMM2 rides along in the routed one.
+  const bool fuse_down = packed && c.n_shared && c.I_shared == c.I && q8;
+  const bool own = c.n_shared && !fuse && !fuse_down;  // the shared expert as a separate FFN
+  const bool two = own && s_aux && s_aux != s_main;
   StreamEvents* ev = nullptr;
   if (two) {
     // fork: the shared expert on s_aux may start once x is ready on s_main
@@ -656,25 +662,39 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     return hip_fail(e, "route");
   // the dispatch also zeroes the routed FFN's 16 tile-queue heads (packed weights)
   if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main, packed ? queues : nullptr,
-                        packed ? 16 : 0)) != hipSuccess)
+                        packed ? (fuse_down ? 24 : 16) : 0)) != hipSuccess)
     return hip_fail(e, "dispatch");
   int8_t* const qcodes = reinterpret_cast<int8_t*>(w + L.qcodes);
   float* const qscales = reinterpret_cast<float*>(w + L.qscales);
   if (q8 && (e = moe::launch_quantize(x, qcodes, qscales, T, c.d, f8, s_main)) != hipSuccess)
     return hip_fail(e, "quantize");
   FusedShared fs;
-  if (fuse) {
-    fs.w_gate_up = ws_gate;
+  if (fuse || fuse_down) {
+    fs.w_gate_up = fuse ? ws_gate : nullptr;
     fs.w_down = ws_down;
     fs.h = w + L.shared_h;
     fs.out = shared;
   }
+  if (fuse_down) {  // the shared expert's GEMM1 on its own (queue heads 16..23, zeroed by the dispatch)
+    moe::GemmProblem g{};
+    g.A = x;
+    g.a_rows = T;
+    g.groups = 1;
+    g.M = T;
+    g.B0 = ws_gate;
+    g.N = c.I_shared;
+    g.K = c.d;
+    g.C = fs.h;
+    g.ldc = c.I_shared;
+    g.tile_queue = queues + 16;
+    if ((e = moe::launch_gemm_stream(g, moe::EPI_SWIGLU, s_main)) != hipSuccess) return hip_fail(e, "shared GEMM1");
+  }
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
-                   w_down, w + L.h, y, s_main, packed, fuse ? &fs : nullptr, queues, q8 ? qscales : nullptr, nullptr,
-                   0, f8, /*queues_zeroed=*/true)) !=
+                   w_down, w + L.h, y, s_main, packed, (fuse || fuse_down) ? &fs : nullptr, queues,
+                   q8 ? qscales : nullptr, nullptr, 0, f8, /*queues_zeroed=*/true)) !=
       hipSuccess)
     return hip_fail(e, "expert FFN");
-  if (c.n_shared && !fuse) {
+  if (own) {
     if (two) {
       if ((e = hipStreamWaitEvent(s_main, ev->join, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     } else if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h,
