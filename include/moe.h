@@ -266,7 +266,9 @@ int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const in
  *           With cfg->token_quant MOE_QUANT_INT8 or MOE_QUANT_FP8 the tokens are quantized
  *           first (moe_quantize, into the workspace) and the routed experts
  *           run on the codes (moe_expert_ffn_q8); the gate and the shared
- *           expert use x, and the shared expert is then not fused.
+ *           expert use x. With packed weights and I_shared == I the shared
+ *           expert's GEMM1 then runs on its own on s_main and its GEMM2
+ *           inside the routed GEMM2.
  *  out    : [T][d] dtype out.
  *  dbg    : NULL, or device buffers to receive intermediates (see above).
  * On return, s_main carries all the work (s_aux is joined into it).
