@@ -38,7 +38,7 @@ def _codes_buf(mode, T, d):
 
 
 @pytest.mark.parametrize("mode", ["int8", "fp8"])
-@pytest.mark.parametrize("T,d", [(1, 64), (37, 256), (300, 7168), (4096, 7168)])
+@pytest.mark.parametrize("T,d", [(1, 64), (37, 256), (300, 7168), (4096, 7168), (5, 8192), (7, 8256)])
 def test_quantize_bit_exact(T, d, mode):
     log("quantize", mode, T, d)
     rng = np.random.default_rng(T + d)
