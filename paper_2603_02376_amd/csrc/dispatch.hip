@@ -47,7 +47,12 @@ __global__ void __launch_bounds__(64 * kWaves) dispatch_count_kernel(DispatchPar
 
 // One workgroup of 1024 threads: thread (part, e) with part in [0, 4) scans a
 // quarter of the chunks for expert e; the four partial sums are combined
-// through LDS.
+// through LDS. Up to kScanRegs chunks per thread (T <= 4096 tokens) the
+// popcounts are loaded once, all loads in flight together, and kept in
+// registers for the second pass; more chunks take a loop that reads the
+// masks twice.
+constexpr int kScanRegs = 16;
+
 __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
   __shared__ int part_sum[4][256];
   __shared__ int wsum[16];
@@ -57,8 +62,16 @@ __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
   const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;
   const int per = (nchunks + 3) / 4;
   const int c0 = part * per, c1 = min(nchunks, c0 + per);
+  const bool regs = per <= kScanRegs;
+  int pc[kScanRegs];
   int run = 0;
-  if (e < p.E) {
+  if (regs) {
+#pragma unroll
+    for (int i = 0; i < kScanRegs; ++i) {
+      pc[i] = (e < p.E && c0 + i < c1) ? __popcll(p.masks[(size_t)(c0 + i) * p.E + e]) : 0;
+      run += pc[i];
+    }
+  } else if (e < p.E) {
     for (int c = c0; c < c1; ++c) run += __popcll(p.masks[(size_t)c * p.E + e]);
   }
   part_sum[part][e] = run;
@@ -71,10 +84,20 @@ __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
     cnt += v;
   }
   if (e < p.E) {
-    for (int c = c0; c < c1; ++c) {
-      const size_t i = (size_t)c * p.E + e;
-      p.bases[i] = base;
-      base += __popcll(p.masks[i]);
+    if (regs) {
+#pragma unroll
+      for (int i = 0; i < kScanRegs; ++i) {
+        if (c0 + i < c1) {
+          p.bases[(size_t)(c0 + i) * p.E + e] = base;
+          base += pc[i];
+        }
+      }
+    } else {
+      for (int c = c0; c < c1; ++c) {
+        const size_t i = (size_t)c * p.E + e;
+        p.bases[i] = base;
+        base += __popcll(p.masks[i]);
+      }
     }
   }
   // exclusive scan of the counts over experts (threads of part 0)

@@ -87,6 +87,7 @@ def test_route_all_equal_logits():
 
 
 @pytest.mark.parametrize("T,d,E,dtype", [(1, 128, 8, "bf16"), (300, 4096, 8, "bf16"), (129, 7168, 256, "bf16"),
+                                         (2050, 7168, 256, "bf16"), (4100, 7168, 256, "bf16"),  # 64-row tiles, ragged
                                          (64, 128, 8, "f32"), (77, 256, 40, "f32")])
 def test_gate_logits(T, d, E, dtype):
     log("gate", T, d, E, dtype)
@@ -125,7 +126,8 @@ def _random_topk(T, E, k, rng, hot=None, pool=None):
 
 @pytest.mark.parametrize("T,E,k,hot", [(1, 8, 2, None), (3, 5, 2, None), (64, 8, 2, None), (65, 8, 8, None),
                                        (1000, 64, 4, None), (4096, 256, 8, None), (4096, 256, 8, 17),
-                                       (777, 256, 1, None), (128, 256, 8, None), (5000, 16, 16, 3)])
+                                       (777, 256, 1, None), (128, 256, 8, None), (5000, 16, 16, 3),
+                                       (4097, 256, 8, None)])
 def test_dispatch_bit_exact(T, E, k, hot):
     log("dispatch", T, E, k, hot)
     rng = np.random.default_rng(T + E + k)
