@@ -26,6 +26,16 @@ namespace {
 
 constexpr int kWaves = 4;  // chunks per workgroup
 
+// A token's expert choices are read kSlotBatch at a time with unconditional
+// loads (slot indices clamped to k - 1; the caller drops slots >= k), so the
+// loads of a batch are in flight together rather than one after another.
+constexpr int kSlotBatch = 8;
+
+__device__ __forceinline__ void load_slots(const DispatchParams& p, int t, int jb, int (&ev)[kSlotBatch]) {
+#pragma unroll
+  for (int j = 0; j < kSlotBatch; ++j) ev[j] = p.topk_idx[(size_t)t * p.k + min(jb + j, p.k - 1)];
+}
+
 __global__ void __launch_bounds__(64 * kWaves) dispatch_count_kernel(DispatchParams p) {
   __shared__ unsigned long long m[kWaves][256];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -35,9 +45,12 @@ __global__ void __launch_bounds__(64 * kWaves) dispatch_count_kernel(DispatchPar
   for (int e = lane; e < p.E; e += 64) m[wave][e] = 0ull;
   __syncthreads();
   if (chunk < nchunks && t < p.T) {
-    for (int j = 0; j < p.k; ++j) {
-      const int e = p.topk_idx[(size_t)t * p.k + j];
-      if ((unsigned)e < (unsigned)p.E) atomicOr(&m[wave][e], 1ull << lane);
+    for (int jb = 0; jb < p.k; jb += kSlotBatch) {
+      int ev[kSlotBatch];
+      load_slots(p, t, jb, ev);
+#pragma unroll
+      for (int j = 0; j < kSlotBatch; ++j)
+        if (jb + j < p.k && (unsigned)ev[j] < (unsigned)p.E) atomicOr(&m[wave][ev[j]], 1ull << lane);
     }
   }
   __syncthreads();
@@ -47,11 +60,20 @@ __global__ void __launch_bounds__(64 * kWaves) dispatch_count_kernel(DispatchPar
 
 // One workgroup of 1024 threads: thread (part, e) with part in [0, 4) scans a
 // quarter of the chunks for expert e; the four partial sums are combined
-// through LDS. Up to kScanRegs chunks per thread (T <= 4096 tokens) the
-// popcounts are loaded once, all loads in flight together, and kept in
-// registers for the second pass; more chunks take a loop that reads the
-// masks twice.
-constexpr int kScanRegs = 16;
+// through LDS. Masks are read in batches of kScanBatch chunks whose loads are
+// unconditional (indices clamped into the thread's range, popcounts past it
+// dropped), so a batch's loads are all in flight together. Up to one batch
+// per thread (T <= 4096 tokens) the popcounts stay in registers for the
+// second pass; beyond that the second pass reads the masks again.
+constexpr int kScanBatch = 16;
+
+__device__ __forceinline__ void scan_batch(const DispatchParams& p, int e, int cb, int c1, int (&pc)[kScanBatch]) {
+  unsigned long long m[kScanBatch];
+#pragma unroll
+  for (int i = 0; i < kScanBatch; ++i) m[i] = p.masks[(size_t)min(cb + i, c1 - 1) * p.E + e];
+#pragma unroll
+  for (int i = 0; i < kScanBatch; ++i) pc[i] = (cb + i < c1) ? __popcll(m[i]) : 0;
+}
 
 __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
   __shared__ int part_sum[4][256];
@@ -62,17 +84,16 @@ __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
   const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;
   const int per = (nchunks + 3) / 4;
   const int c0 = part * per, c1 = min(nchunks, c0 + per);
-  const bool regs = per <= kScanRegs;
-  int pc[kScanRegs];
+  const bool active = e < p.E && c0 < c1;  // c1 - 1 is then a valid chunk
+  const bool regs = per <= kScanBatch;
+  int pc[kScanBatch];
   int run = 0;
-  if (regs) {
+  if (active) {
+    for (int cb = c0; cb < c1; cb += kScanBatch) {
+      scan_batch(p, e, cb, c1, pc);
 #pragma unroll
-    for (int i = 0; i < kScanRegs; ++i) {
-      pc[i] = (e < p.E && c0 + i < c1) ? __popcll(p.masks[(size_t)(c0 + i) * p.E + e]) : 0;
-      run += pc[i];
+      for (int i = 0; i < kScanBatch; ++i) run += pc[i];
     }
-  } else if (e < p.E) {
-    for (int c = c0; c < c1; ++c) run += __popcll(p.masks[(size_t)c * p.E + e]);
   }
   part_sum[part][e] = run;
   __syncthreads();
@@ -83,20 +104,15 @@ __global__ void __launch_bounds__(1024) dispatch_scan_kernel(DispatchParams p) {
     if (q < part) base += v;
     cnt += v;
   }
-  if (e < p.E) {
-    if (regs) {
+  if (active) {
+    for (int cb = c0; cb < c1; cb += kScanBatch) {
+      if (!regs) scan_batch(p, e, cb, c1, pc);  // one batch: pc still holds it
 #pragma unroll
-      for (int i = 0; i < kScanRegs; ++i) {
-        if (c0 + i < c1) {
-          p.bases[(size_t)(c0 + i) * p.E + e] = base;
+      for (int i = 0; i < kScanBatch; ++i) {
+        if (cb + i < c1) {
+          p.bases[(size_t)(cb + i) * p.E + e] = base;
           base += pc[i];
         }
-      }
-    } else {
-      for (int c = c0; c < c1; ++c) {
-        const size_t i = (size_t)c * p.E + e;
-        p.bases[i] = base;
-        base += __popcll(p.masks[i]);
       }
     }
   }
@@ -131,15 +147,28 @@ __global__ void __launch_bounds__(64 * kWaves) dispatch_scatter_kernel(DispatchP
   const int t = chunk * kDispatchChunk + lane;
   if (t >= p.T) return;
   const unsigned long long below = (1ull << lane) - 1ull;
-  for (int j = 0; j < p.k; ++j) {
-    const int a = t * p.k + j;
-    const int e = p.topk_idx[a];
-    if ((unsigned)e >= (unsigned)p.E) continue;  // invalid input: row left unassigned
-    const size_t ci = (size_t)chunk * p.E + e;
-    const int row = p.offsets[e] + p.bases[ci] + __popcll(p.masks[ci] & below);
-    p.sorted_token[row] = t;
-    if (p.sorted_assign) p.sorted_assign[row] = a;
-    p.inv_perm[a] = row;
+  for (int jb = 0; jb < p.k; jb += kSlotBatch) {
+    int ev[kSlotBatch], off[kSlotBatch], base[kSlotBatch];
+    unsigned long long mk[kSlotBatch];
+    load_slots(p, t, jb, ev);
+#pragma unroll
+    for (int j = 0; j < kSlotBatch; ++j) {  // every load of the batch issued before any use
+      const int ec = min(max(ev[j], 0), p.E - 1);
+      const size_t ci = (size_t)chunk * p.E + ec;
+      off[j] = p.offsets[ec];
+      base[j] = p.bases[ci];
+      mk[j] = p.masks[ci];
+    }
+#pragma unroll
+    for (int j = 0; j < kSlotBatch; ++j) {
+      // slots past k, and invalid expert ids (row left unassigned), are dropped
+      if (jb + j >= p.k || (unsigned)ev[j] >= (unsigned)p.E) continue;
+      const int a = t * p.k + jb + j;
+      const int row = off[j] + base[j] + __popcll(mk[j] & below);
+      p.sorted_token[row] = t;
+      if (p.sorted_assign) p.sorted_assign[row] = a;
+      p.inv_perm[a] = row;
+    }
   }
 }
 
