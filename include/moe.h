@@ -168,6 +168,12 @@ int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
  *  sorted_assign : [T*k] out or NULL, assignment of every row.
  *  inv_perm      : [T*k] out, row of every assignment.
  *  ws            : workspace (per-chunk expert masks and bases).
+ * Every row of topk_idx is expected to hold k distinct experts in [0, E), as
+ * moe_route writes them. An id outside [0, E) is skipped: its assignment gets
+ * no row (its inv_perm entry is not written), offsets[E] counts only the
+ * valid assignments, and rows past offsets[E] are not written. An expert
+ * repeated within one row gives unspecified rows, but never an access out of
+ * bounds.
  */
 int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, int32_t* counts,
                  int32_t* offsets, int32_t* sorted_token, int32_t* sorted_assign,

@@ -127,7 +127,7 @@ def _random_topk(T, E, k, rng, hot=None, pool=None):
 @pytest.mark.parametrize("T,E,k,hot", [(1, 8, 2, None), (3, 5, 2, None), (64, 8, 2, None), (65, 8, 8, None),
                                        (1000, 64, 4, None), (4096, 256, 8, None), (4096, 256, 8, 17),
                                        (777, 256, 1, None), (128, 256, 8, None), (5000, 16, 16, 3),
-                                       (4097, 256, 8, None)])
+                                       (4097, 256, 8, None), (999, 64, 6, None), (2000, 256, 12, None)])
 def test_dispatch_bit_exact(T, E, k, hot):
     log("dispatch", T, E, k, hot)
     rng = np.random.default_rng(T + E + k)
@@ -143,6 +143,35 @@ def test_dispatch_bit_exact(T, E, k, hot):
     for name, g, w in zip(("counts", "offsets", "sorted_token", "sorted_assign", "inv_perm"), outs, want):
         assert np.array_equal(host(g), w), name
     check_dispatch(idx, *(host(o) for o in (outs[0], outs[1], outs[2], outs[4], outs[3])))
+
+
+@pytest.mark.parametrize("T,E,k", [(300, 64, 6), (4096, 256, 8), (70, 16, 12)])
+def test_dispatch_skips_invalid_ids(T, E, k):
+    """Ids outside [0, E) get no row; the valid assignments are grouped by
+    expert exactly as if the invalid ones were absent (stable order by
+    assignment), and nothing past the valid rows is written."""
+    log("dispatch invalid ids", T, E, k)
+    rng = np.random.default_rng(7 * T + k)
+    idx = _random_topk(T, E, k, rng)
+    bad = rng.random(idx.shape) < 0.1
+    idx[bad] = rng.choice(np.array([-1, E, E + 5, -(1 << 30)], dtype=np.int32), size=int(bad.sum()))
+    cfg = moe.MoeConfig(d=64, E=E, k=k, I=64, dtype="bf16")
+    ws = moe.alloc_workspace(cfg, T)
+    outs = [torch.full((n,), -7, dtype=torch.int32, device="cuda") for n in (E, E + 1, T * k, T * k, T * k)]
+    moe.moe_dispatch(cfg, T, _dev(idx), *outs, ws)
+    torch.cuda.synchronize()
+    counts, offsets, st, sa, inv = (host(o) for o in outs)
+    flat = idx.reshape(-1)
+    valid = np.flatnonzero((flat >= 0) & (flat < E))
+    order = valid[np.argsort(flat[valid], kind="stable")]   # assignments by expert, then by assignment
+    n = len(order)
+    assert np.array_equal(counts, np.bincount(flat[valid], minlength=E))
+    assert np.array_equal(offsets, np.concatenate([[0], np.cumsum(counts)]))
+    assert np.array_equal(sa[:n], order) and np.array_equal(st[:n], order // k)
+    assert (sa[n:] == -7).all() and (st[n:] == -7).all()
+    want_inv = np.full(T * k, -7)
+    want_inv[order] = np.arange(n)
+    assert np.array_equal(inv, want_inv)
 
 
 # ---------------------------------------------------------------------------
