@@ -125,18 +125,30 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
   // ---- scores and keys ---------------------------------------------------
   double key[EPL], score[EPL];
   float u[EPL], bv[EPL];
-  // Logits: the K-split partials summed in ascending split order. Each
-  // round issues the loads of up to 8 splits for all of the lane's experts
-  // before adding them, so the loads overlap instead of waiting one by one.
-  // The selection bias is loaded with them (not inside the score loop, where
-  // every load would be waited for on its own).
+  // Logits: the K-split partials summed in ascending split order. The first
+  // split and the selection bias are loaded unconditionally, from indices
+  // clamped into range, and dropped afterwards where they do not count (a
+  // load under its own condition is waited for on its own). Each later round
+  // issues the loads of up to 8 splits for all of the lane's experts before
+  // adding them; those loads keep their conditions (clamped loads of the
+  // splits past the last measured slower).
   {
     constexpr int R = 8;
+    const size_t trow = (size_t)min(t, p.T - 1) * E;
+    int ec[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) ec[i] = min(lane * EPL + i, E - 1);
+    const float* const bias = p.bias ? p.bias : p.logits_in;  // any valid address when there is no bias
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      u[i] = p.logits_in[trow + ec[i]];
+      bv[i] = bias[ec[i]];
+    }
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
       const int e = lane * EPL + i;
-      u[i] = (active && e < E) ? p.logits_in[(size_t)t * E + e] : 0.f;
-      bv[i] = (p.bias && e < E) ? p.bias[e] : 0.f;
+      if (!(active && e < E)) u[i] = 0.f;
+      if (!(p.bias && e < E)) bv[i] = 0.f;
     }
     for (int sp0 = 1; sp0 < p.nsplit; sp0 += R) {
       float part[R][EPL];
@@ -146,7 +158,7 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
         for (int i = 0; i < EPL; ++i) {
           const int e = lane * EPL + i;
           part[q][i] = (active && e < E && sp0 + q < p.nsplit)
-                           ? p.logits_in[(size_t)(sp0 + q) * p.split_stride + (size_t)t * E + e]
+                           ? p.logits_in[(size_t)(sp0 + q) * p.split_stride + trow + e]
                            : 0.f;
         }
 #pragma unroll
