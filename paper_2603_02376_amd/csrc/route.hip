@@ -22,7 +22,10 @@
 namespace moe {
 namespace {
 
-constexpr int kWaves = 4;
+// Tokens (one wave each) per workgroup. One: a small batch spreads over as
+// many compute units as it has tokens (128 tokens: 19.6 us against 23.2 with
+// four per workgroup, router GEMM included), and 4096 tokens lose nothing.
+constexpr int kWaves = 1;
 
 struct KeyIdx {
   double key;
