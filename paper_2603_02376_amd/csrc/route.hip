@@ -22,10 +22,12 @@
 namespace moe {
 namespace {
 
-// Tokens (one wave each) per workgroup. One: a small batch spreads over as
-// many compute units as it has tokens (128 tokens: 19.6 us against 23.2 with
-// four per workgroup, router GEMM included), and 4096 tokens lose nothing.
-constexpr int kWaves = 1;
+// Tokens (one wave each) per workgroup, chosen per launch: one below
+// kOneWaveTokens tokens, so a small batch spreads over as many compute units
+// as it has tokens (128 tokens: 12.6 us in the layer against 18.0 with four
+// per workgroup); four from there up, where single-wave workgroups made the
+// kernel slower (4096 tokens: 27.2 us against 24-25).
+constexpr int kOneWaveTokens = 1024;
 
 struct KeyIdx {
   double key;
@@ -116,7 +118,7 @@ __device__ __forceinline__ void top2_step(double& m1, double& m2) {
   m2 = n2;
 }
 
-template <int EPL>
+template <int EPL, int kWaves>
 __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
   __shared__ double skeys[kWaves][256];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -324,17 +326,26 @@ __global__ void __launch_bounds__(64 * kWaves) route_kernel(RouteParams p) {
   }
 }
 
+template <int W>
+void launch_epl(const RouteParams& p, int epl, hipStream_t s) {
+  const dim3 grid((p.T + W - 1) / W), block(64 * W);
+  switch (epl) {
+    case 1: hipLaunchKernelGGL((route_kernel<1, W>), grid, block, 0, s, p); break;
+    case 2: hipLaunchKernelGGL((route_kernel<2, W>), grid, block, 0, s, p); break;
+    case 3: hipLaunchKernelGGL((route_kernel<3, W>), grid, block, 0, s, p); break;
+    default: hipLaunchKernelGGL((route_kernel<4, W>), grid, block, 0, s, p); break;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_route(const RouteParams& p, hipStream_t s) {
   if (p.T <= 0) return hipSuccess;
-  const dim3 grid((p.T + kWaves - 1) / kWaves), block(64 * kWaves);
   const int epl = (p.E + 63) / 64;
-  switch (epl) {
-    case 1: hipLaunchKernelGGL(route_kernel<1>, grid, block, 0, s, p); break;
-    case 2: hipLaunchKernelGGL(route_kernel<2>, grid, block, 0, s, p); break;
-    case 3: hipLaunchKernelGGL(route_kernel<3>, grid, block, 0, s, p); break;
-    default: hipLaunchKernelGGL(route_kernel<4>, grid, block, 0, s, p); break;
+  if (p.T < kOneWaveTokens) {
+    launch_epl<1>(p, epl, s);
+  } else {
+    launch_epl<4>(p, epl, s);
   }
   return hipGetLastError();
 }
