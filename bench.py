@@ -11,8 +11,9 @@ weight-streaming expert GEMMs then read them, and the shared expert runs
 inside them as one more group. --layout rowmajor times the tiled GEMMs on
 the plain [E][I][d] weights instead. Prints ONE JSON line: tokens/s of the
 layer, the roofline of the dominant kernel pair (the grouped expert FFN,
-timed with HIP events on its own stream), the CPU oracle timed on a bounded
-sample of the same workload as a baseline, the per-layer time of 1, 4 and 16
+timed with HIP events on its own stream), the CPU oracle timed on the same
+workload (all tokens routed and combined, a seeded subset of whole experts
+run and the rest of the expert FFN scaled from them) as a baseline, the per-layer time of 1, 4 and 16
 layer calls run back to back, the layer with the shared expert inside the
 routed GEMMs against the same layer composed from the public calls with the
 shared expert on one or two streams, the receive side of two-GPU expert parallelism
@@ -82,6 +83,7 @@ def measured_traffic(workload: str, layout: str):
     return rec.get("bytes_per_call")
 
 
+CPU_EXPERTS = 64  # whole experts the CPU baseline runs; the rest of the expert FFN is scaled from them
 EP_LINK_WORKGROUPS = 16  # workgroups of the emulated exchange (~77 GB/s measured: about one xGMI link, one way)
 EP_CHUNKS = (4, 8, 16)
 
@@ -179,7 +181,7 @@ def ep_split(p: dict, x, gate_up, down, steps: int, warmup: int) -> dict:
                      "link_workgroups workgroups on its own stream; speedups are over the sequential schedule")
 
 
-def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens: int = 64,
+def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_experts: int = CPU_EXPERTS,
                  ffn_only: bool = False, layout: str = "packed", multilayer: tuple = (), int8: bool = False,
                  ep: bool = False):
     import numpy as np
@@ -400,51 +402,73 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_tokens:
         multilayer_ms_per_layer=ml,
     )
     if want_cpu:
-        log(f"[bench] {name}: CPU oracle baseline on {cpu_tokens} tokens")
-        res["cpu"] = cpu_baseline(p, t, cpu_tokens)
+        log(f"[bench] {name}: CPU oracle baseline ({cpu_experts} whole experts, all tokens routed)")
+        res["cpu"] = cpu_baseline(p, t, cpu_experts)
     del t, ws, out, y, w_ffn, w_sh
     torch.cuda.empty_cache()
     return res
 
 
-def cpu_baseline(p, t, n_tokens: int = 16):
-    """The oracle, as it stands, on the first n_tokens tokens of the workload:
-    gate logits, routing, every selected expert's SwiGLU FFN, shared expert and
-    combine, all in fp64 on the host cores. The weights of the experts those
-    tokens use are copied to host memory before the clock starts."""
+def cpu_baseline(p, t, n_experts: int = CPU_EXPERTS):
+    """The oracle, as it stands, timed on the host cores over the whole
+    workload's routing and a seeded subset of whole experts: gate logits and
+    routing of all T tokens, dispatch, the SwiGLU FFN of every row of
+    n_experts of the touched experts (a seeded choice), the shared expert on
+    all T tokens, and the combine of all tokens, everything in fp64. The
+    expert-FFN time is scaled by touched / n_experts (every touched expert of
+    a uniformly routed workload has about the same rows); the rest is timed
+    whole. The sampled experts' weights are copied to host RAM before the
+    clock starts (their bf16 -> fp64 conversion is timed)."""
     import numpy as np
 
     from oracle import moe_oracle as O
     from paper_2603_02376_amd import inputs
 
-    rows = np.arange(min(n_tokens, p["T"]))
+    T, E = p["T"], p["E"]
     x = inputs.oracle_view(t["x"])
     wr = inputs.oracle_view(t["w_router"])
     bias = None if p["score"] == "softmax" else inputs.oracle_view(t["bias"])
-    # experts the sample needs: route once before the clock starts, copy their weights to host RAM
     kw = dict(k=p["k"], score=p["score"], bias=bias, n_groups=p["n_groups"], topk_groups=p["topk_groups"],
               renorm=p["renorm"], scale=p["scale"])
-    need = np.unique(O.route(O.gate_logits(x[rows], wr), **kw)[0])
-    host_w = {n: {int(e): inputs.oracle_view(t[n][int(e)]) for e in need} for n in ("w_gate", "w_up", "w_down")}
-    sh = [inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")] if p["n_shared"] else [None] * 3
+    # the sampled experts: routed once before the clock starts, their weights copied to host RAM
+    touched = np.nonzero(O.dispatch(O.route(O.gate_logits(x, wr), **kw)[0], E)[0])[0]
+    rng = np.random.default_rng(0)
+    chosen = np.sort(rng.choice(touched, min(n_experts, touched.size), replace=False))
+    host_w = {n: {int(e): inputs.oracle_view(t[n][int(e)]) for e in chosen} for n in ("w_gate", "w_up", "w_down")}
+    sh = [inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")] if p["n_shared"] else None
 
     t0 = time.perf_counter()
-    logits = O.gate_logits(x[rows], wr)
-    idx, w = O.route(logits, **kw)
-    O.layer_rows(x, rows, idx, w, host_w["w_gate"], host_w["w_up"], host_w["w_down"], *sh)
-    dt = time.perf_counter() - t0
-    threads = None
+    idx, w = O.route(O.gate_logits(x, wr), **kw)
+    counts, offsets, st, _, inv = O.dispatch(idx, E)
+    t1 = time.perf_counter()
+    y = np.zeros((int(offsets[-1]), p["d"]))   # rows of the experts not run stay 0 (their time is scaled in)
+    for e in chosen:
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        y[lo:hi] = O.swiglu_ffn(x[st[lo:hi]], host_w["w_gate"][int(e)], host_w["w_up"][int(e)],
+                                host_w["w_down"][int(e)])
+    t2 = time.perf_counter()
+    shared = O.swiglu_ffn(x, *sh) if sh else None
+    O.combine(y, inv, w, shared)
+    t3 = time.perf_counter()
+    n_touched = int((counts > 0).sum())
+    est = (t1 - t0) + (t2 - t1) * n_touched / len(chosen) + (t3 - t2)
+    blas, threads = "unknown", None
     try:
         from threadpoolctl import threadpool_info
 
-        threads = max((i.get("num_threads", 0) for i in threadpool_info()), default=None)
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')} ({info[0].get('architecture')})"
+            threads = info[0].get("num_threads")
     except Exception:
         pass
-    return dict(value=len(rows) / dt, unit="tokens/s", cores=threads or len(os.sched_getaffinity(0)),
-                kind="oracle", seconds=dt,
-                sample=f"first {len(rows)} of {p['T']} tokens of the {p.get('name')} workload: gate, routing, "
-                       f"{len(need)} routed experts' SwiGLU FFN{', shared expert' if p['n_shared'] else ''} "
-                       f"and combine in fp64 (weights pre-copied to host RAM)")
+    return dict(value=T / est, unit="tokens/s", cores=threads or len(os.sched_getaffinity(0)),
+                host_cpus=len(os.sched_getaffinity(0)), blas=blas, kind="oracle", seconds_timed=t3 - t0,
+                seconds_layer_estimate=est,
+                sample=f"the {p.get('name')} workload (T={T}): gate, routing, dispatch and combine of all {T} tokens"
+                       f"{', the shared expert on all of them' if sh else ''}, and the SwiGLU FFN of every row of "
+                       f"{len(chosen)} of the {n_touched} touched experts (seeded choice), in fp64; the expert-FFN "
+                       f"time scaled by {n_touched}/{len(chosen)} to the whole layer")
 
 
 def main():
@@ -457,7 +481,8 @@ def main():
                     help="routed-expert weight layout (packed: converted once before timing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the side measurements (other workloads, multi-layer)")
-    ap.add_argument("--cpu-tokens", type=int, default=64, help="tokens in the CPU-oracle baseline sample")
+    ap.add_argument("--cpu-experts", type=int, default=CPU_EXPERTS,
+                    help="whole experts the CPU-oracle baseline runs (the rest of its expert FFN is scaled)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run 3 plain device copies of this many MiB (reference for HBM byte counters)")
     ap.add_argument("--ffn-only", action="store_true",
@@ -486,7 +511,7 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] copy calibration: 3 x {n} B, {2 * 3 * n / (c0.elapsed_time(c1) / 1e3) / 1e9:.1f} GB/s")
         del src, dst
-    main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_tokens,
+    main_res = run_workload(args.workload, args.steps, args.warmup, not args.no_cpu_baseline, args.cpu_experts,
                             args.ffn_only, args.layout, multilayer=() if args.no_extra else (1, 4, 16),
                             int8=not args.no_extra, ep=not args.no_extra)
     if args.ffn_only:

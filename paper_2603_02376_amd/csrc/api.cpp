@@ -27,6 +27,12 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(MOE_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Every launch helper reports hipGetLastError() after its launch. An error
+// left pending by earlier, unrelated work on this thread would otherwise be
+// reported as this call's failure, so each entry point clears it once its
+// arguments are validated, right before its first HIP call.
+void clear_pending_error() { (void)hipGetLastError(); }
+
 constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -336,9 +342,17 @@ hipError_t run_combine(const moe_config_t& c, int32_t T, const void* y, const in
   return moe::launch_combine(p, c.dtype == MOE_BF16, s);
 }
 
-// Two events per (thread, device) for the fork/join of moe_layer's streams.
+// Two events per (thread, device) for the fork/join of moe_layer's streams,
+// created on first use and destroyed when the thread ends.
 struct StreamEvents {
   hipEvent_t fork = nullptr, join = nullptr;
+  StreamEvents() = default;
+  StreamEvents(const StreamEvents&) = delete;
+  StreamEvents& operator=(const StreamEvents&) = delete;
+  ~StreamEvents() {
+    if (fork) (void)hipEventDestroy(fork);
+    if (join) (void)hipEventDestroy(join);
+  }
 };
 
 hipError_t layer_events(StreamEvents** out) {
@@ -348,11 +362,9 @@ hipError_t layer_events(StreamEvents** out) {
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   StreamEvents& se = ev[dev];
-  if (!se.fork) {
-    e = hipEventCreateWithFlags(&se.fork, hipEventDisableTiming);
-    if (e != hipSuccess) return e;
-    e = hipEventCreateWithFlags(&se.join, hipEventDisableTiming);
-    if (e != hipSuccess) return e;
+  if (!se.join) {
+    if (!se.fork && (e = hipEventCreateWithFlags(&se.fork, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&se.join, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &se;
   return hipSuccess;
@@ -364,6 +376,14 @@ constexpr int kEpMaxChunks = 16;
 struct EpEvents {
   hipEvent_t fork = nullptr;
   hipEvent_t chunk[kEpMaxChunks] = {};
+  EpEvents() = default;
+  EpEvents(const EpEvents&) = delete;
+  EpEvents& operator=(const EpEvents&) = delete;
+  ~EpEvents() {
+    for (hipEvent_t c : chunk)
+      if (c) (void)hipEventDestroy(c);
+    if (fork) (void)hipEventDestroy(fork);
+  }
 };
 
 hipError_t ep_events(EpEvents** out) {
@@ -373,9 +393,9 @@ hipError_t ep_events(EpEvents** out) {
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   EpEvents& se = ev[dev];
-  if (!se.fork) {
+  if (!se.fork) {  // the fork last: set once every event exists
     for (int i = 0; i < kEpMaxChunks; ++i)
-      if ((e = hipEventCreateWithFlags(&se.chunk[i], hipEventDisableTiming)) != hipSuccess) return e;
+      if (!se.chunk[i] && (e = hipEventCreateWithFlags(&se.chunk[i], hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&se.fork, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &se;
@@ -472,6 +492,7 @@ int moe_route(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   }
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   float* partials = x ? reinterpret_cast<float*>(static_cast<char*>(ws) + make_layout(*cfg, T).gate_partials) : nullptr;
   const hipError_t e = run_gate_route(*cfg, T, x, w_router, bias, logits, partials, topk_idx, topk_w, stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "route");
@@ -489,6 +510,7 @@ int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, in
   if (sorted_assign && !aligned16(sorted_assign)) return fail(MOE_ERR_INVALID_ARG, "sorted_assign is not 16-byte aligned");
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_dispatch(*cfg, T, topk_idx, static_cast<char*>(ws), L, counts, offsets, sorted_token,
                                     sorted_assign, inv_perm, stream);
@@ -509,6 +531,7 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   MOE_CHECK(need(y_perm, "y_perm"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
                                static_cast<char*>(ws) + L.h, y_perm, stream, packed, nullptr,
@@ -531,6 +554,7 @@ int moe_quantize(const moe_config_t* cfg, int32_t T, const void* x, int8_t* code
   MOE_CHECK(need(codes, "codes"));
   MOE_CHECK(need(scales, "scales"));
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   const hipError_t e =
       moe::launch_quantize(x, codes, scales, T, cfg->d, cfg->token_quant == MOE_QUANT_FP8, stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "quantize");
@@ -551,6 +575,7 @@ int moe_expert_ffn_q8(const moe_config_t* cfg, int32_t T, const int8_t* codes, c
   MOE_CHECK(need(y_perm, "y_perm"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, codes, sorted_token, offsets, w_gate_up, nullptr,
                                w_down, static_cast<char*>(ws) + L.h, y_perm, stream, true, nullptr,
@@ -571,6 +596,7 @@ int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void
   MOE_CHECK(need(out, "out"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T, 1, cfg->I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down,
                                static_cast<char*>(ws) + L.shared_h, out, stream, packed, nullptr,
@@ -587,6 +613,7 @@ int moe_combine(const moe_config_t* cfg, int32_t T, const void* y_perm, const in
   MOE_CHECK(need(out, "out"));
   if (shared_out && !aligned16(shared_out)) return fail(MOE_ERR_INVALID_ARG, "shared_out is not 16-byte aligned");
   if (T == 0) return MOE_OK;
+  clear_pending_error();
   const hipError_t e = run_combine(*cfg, T, y_perm, inv_perm, topk_w, shared_out, out, stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "combine");
 }
@@ -619,6 +646,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     if (p && !aligned16(p)) return fail(MOE_ERR_INVALID_ARG, "debug buffer is not 16-byte aligned");
   if (d.shared_out && !c.n_shared) return fail(MOE_ERR_INVALID_ARG, "debug shared_out without a shared expert");
   if (T == 0) return MOE_OK;
+  clear_pending_error();
 
   const Layout L = make_layout(c, T);
   char* w = static_cast<char*>(ws);
@@ -735,6 +763,7 @@ int moe_ep_plan(const moe_config_t* cfg, int32_t e_first, const int32_t* self_of
   p.row_token = row_token;
   p.offsets = offsets;
   p.self_end = self_end;
+  clear_pending_error();
   const hipError_t e = moe::launch_ep_plan(p, stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "receive plan");
 }
@@ -753,6 +782,7 @@ int moe_ep_copy_rows(const moe_config_t* cfg, int32_t source, int32_t n_rows, co
   if (src_tokens < 0) return fail(MOE_ERR_INVALID_ARG, "src_tokens < 0");
   if (src_tokens > 0) MOE_CHECK(need(x_src, "x_src"));
   if (n_rows == 0 || e_begin == e_end || src_tokens == 0) return MOE_OK;
+  clear_pending_error();
   const hipError_t e = run_ep_copy(*cfg, source, n_rows, x_src, src_tokens, row_token, offsets, self_end, e_begin,
                                    e_end, recv, max_workgroups, stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "row copy");
@@ -773,6 +803,7 @@ int moe_expert_ffn_segments(const moe_config_t* cfg, int32_t n_rows, const void*
   MOE_CHECK(need(y, "y"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (n_rows == 0 || e_begin == e_end) return MOE_OK;
+  clear_pending_error();
   const hipError_t e = run_ffn_segments(*cfg, n_rows, x, seg_begin, seg_end, e_begin, e_end, w_gate_up, w_down, y,
                                         max_workgroups, static_cast<char*>(ws), make_layout(*cfg, T), stream);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
@@ -803,6 +834,7 @@ int moe_ep_expert_ffn(const moe_config_t* cfg, const moe_ep_options_t* opt, int3
   MOE_CHECK(need(y, "y"));
   MOE_CHECK(check_ws(cfg, T, ws, ws_bytes));
   if (n_rows == 0) return MOE_OK;
+  clear_pending_error();
 
   const moe_config_t& c = *cfg;
   const Layout L = make_layout(c, T);
@@ -881,6 +913,8 @@ int moe_pack_weights(const moe_config_t* cfg, const void* w_gate, const void* w_
     MOE_CHECK(need(w_down, "w_down"));
     MOE_CHECK(need(down_packed, "down_packed"));
   }
+  if (!gate_up_packed && !down_packed) return MOE_OK;
+  clear_pending_error();
   hipError_t e;
   if (gate_up_packed && (e = moe::launch_pack(w_gate, w_up, gate_up_packed, c.E, c.I, c.d, true, stream)) != hipSuccess)
     return hip_fail(e, "pack gate/up");

@@ -88,7 +88,9 @@ def run_layer(p: dict, t: dict, s_main=None, s_aux="new", with_debug=True) -> di
     dev = "cuda"
     dt = cfg.torch_dtype
     ws = moe.alloc_workspace(cfg, T)
-    out = torch.empty((T, d), dtype=dt, device=dev)
+    # outputs start as NaN, so a row the kernels never write fails every check
+    nan = float("nan")
+    out = torch.full((T, d), nan, dtype=dt, device=dev)
     dbg = None
     if with_debug:
         dbg = dict(logits=torch.empty((T, E), dtype=torch.float32, device=dev),
@@ -99,9 +101,9 @@ def run_layer(p: dict, t: dict, s_main=None, s_aux="new", with_debug=True) -> di
                    sorted_token=torch.empty(T * k, dtype=torch.int32, device=dev),
                    sorted_assign=torch.empty(T * k, dtype=torch.int32, device=dev),
                    inv_perm=torch.empty(T * k, dtype=torch.int32, device=dev),
-                   y_perm=torch.empty((T * k, d), dtype=dt, device=dev))
+                   y_perm=torch.full((T * k, d), nan, dtype=dt, device=dev))
         if p.get("n_shared", 0):
-            dbg["shared_out"] = torch.empty((T, d), dtype=dt, device=dev)
+            dbg["shared_out"] = torch.full((T, d), nan, dtype=dt, device=dev)
     if s_aux == "new":
         s_aux = torch.cuda.Stream()
     wg, wu, wd = t["w_gate"], t["w_up"], t["w_down"]
@@ -176,3 +178,32 @@ def near_tie_report(p: dict, t: dict, r: dict, rows=None) -> int:
         assert (det["margin"][diff] < NEAR_TIE).all(), \
             f"tokens {diff[:5]} differ from the fp64 routing without a near tie"
     return int(diff.size)
+
+
+def check_expert_segments(x, st, off, wg, wu, wd, experts, ys, tol, quant=None) -> float:
+    """Every row of the listed experts' segments of y_perm against the oracle's
+    SwiGLU FFN of that expert on the same gathered tokens (whole segments, so
+    every pass, column tile and K step of those experts is covered).
+    x: the oracle view of the tokens; st, off: host sorted_token and offsets;
+    wg, wu, wd: per-expert accessors; experts: expert ids; ys: {label: y_perm
+    device tensor} (each compared with the same oracle rows). quant:
+    "int8"/"fp8" when the experts saw quantized tokens."""
+    worst = 0.0
+    for e in experts:
+        lo, hi = int(off[e]), int(off[e + 1])
+        if hi == lo:
+            continue
+        rows = np.asarray(x)[st[lo:hi]]
+        if quant == "int8":
+            rows = O.dequantize_tokens(*O.quantize_tokens(rows))
+        elif quant == "fp8":
+            rows = O.dequantize_tokens_fp8(*O.quantize_tokens_fp8(rows))
+        want = O.swiglu_ffn(rows, wg[e], wu[e], wd[e])
+        for label, y in ys.items():
+            got = host(y[lo:hi].float())
+            assert np.isfinite(got).all(), f"{label} expert {e}: rows left unwritten"
+            err = max_rel_err(got, want)
+            log(f"  {label} expert {e}: {hi - lo} rows, max_rel_err {err:.3e}")
+            assert err <= tol, f"{label} expert {e} ({hi - lo} rows): max_rel_err {err}"
+            worst = max(worst, err)
+    return worst

@@ -149,3 +149,33 @@ def test_zero_tokens_is_a_noop():
     assert L.moe_combine(ctypes.byref(c), 0, FAKE, FAKE, FAKE, None, FAKE, None) == 0
     assert L.moe_layer(ctypes.byref(c), 0, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                        FAKE, need, None, None, None) == 0
+
+
+def test_last_error_is_per_thread():
+    """moe_last_error() holds the message of the calling thread's last failure:
+    a failure on another thread leaves this thread's message alone."""
+    import threading
+
+    L = moe.lib()
+    c = _cfg().c()
+    assert L.moe_route(ctypes.byref(c), -1, None, None, None, FAKE, FAKE, FAKE, None, 0, None) == -1
+    mine = L.moe_last_error()
+    assert b"T < 0" in mine
+    seen = {}
+
+    def other():
+        seen["before"] = L.moe_last_error()
+        seen["status"] = L.moe_route(ctypes.byref(c), 4, None, None, None, None, FAKE, FAKE, None, 0, None)
+        seen["after"] = L.moe_last_error()
+
+    th = threading.Thread(target=other)
+    th.start()
+    th.join()
+    assert seen["before"] == b"" and seen["status"] == -1 and b"logits" in seen["after"]
+    assert L.moe_last_error() == mine
+
+
+def test_pack_weights_with_nothing_to_pack_makes_no_hip_call():
+    # no output buffer: validated and returns before any HIP call (runs without a GPU)
+    c = _cfg(d=256, I=128).c()
+    assert moe.lib().moe_pack_weights(ctypes.byref(c), None, None, None, None, None, None) == 0

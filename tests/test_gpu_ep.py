@@ -284,7 +284,7 @@ def test_ep_full_size_sampled():
     outs = {}
     for sched, chunks in (("sequential", 1), ("self_remote", 1), ("expert_chunks", 4)):
         recv = torch.empty((n, d), dtype=torch.bfloat16, device="cuda")
-        y = torch.empty((n, d), dtype=torch.bfloat16, device="cuda")
+        y = torch.full((n, d), float("nan"), dtype=torch.bfloat16, device="cuda")
         moe.moe_ep_expert_ffn(s["cfg"], sched, n, s["x"], T, s["xp"], T, s["rt"], s["off"], s["se"], s["gu"],
                               s["dn"], recv, y, ws, chunks=chunks, link_workgroups=8,
                               gemm_workgroups=248, s_link=link)
@@ -293,6 +293,7 @@ def test_ep_full_size_sampled():
         del recv
     assert torch.equal(outs["sequential"], outs["self_remote"])
     assert torch.equal(outs["sequential"], outs["expert_chunks"])
+    assert not torch.isnan(outs["sequential"]).any(), "rows left unwritten"
     off, se = host(s["off"]), host(s["se"])
     rows = []
     for e in (0, 1, 63, 127):
@@ -303,5 +304,13 @@ def test_ep_full_size_sampled():
     err = max_rel_err(got, want)
     log("  sampled max_rel_err", err)
     assert err <= BF16_TOL
+    # two whole experts (their self and remote rows: every pass and column tile)
+    for e in (0, int(np.argmax(np.diff(off)))):
+        seg = np.arange(int(off[e]), int(off[e + 1]))
+        want = _oracle_y(s, rows=seg)
+        got = host(outs["sequential"][int(off[e]):int(off[e + 1])].float())
+        err = max_rel_err(got, want)
+        log(f"  expert {e}: {seg.size} rows, max_rel_err {err:.3e}")
+        assert err <= BF16_TOL
     del outs
     torch.cuda.empty_cache()

@@ -44,6 +44,13 @@ ROUTE_CASES = [
     (64, 12, 4, 3, 2, "sigmoid", True, True, 1.0),
     (33, 256, 16, 1, 1, "sigmoid", True, True, 2.5),
     (50, 4, 4, 1, 1, "softmax", False, True, 1.0),       # k = E
+    # from 1024 tokens the kernel takes four tokens per workgroup: ragged last
+    # workgroups (T % 4 != 0) on the group paths, fewer than 4 experts per lane
+    # and one group per lane (the LDS group path)
+    (1027, 96, 5, 4, 2, "sigmoid", True, True, 2.5),
+    (2050, 256, 8, 64, 16, "sigmoid", True, True, 2.5),
+    (1030, 128, 6, 8, 3, "softmax", False, True, 1.0),
+    (1025, 64, 4, 4, 2, "sigmoid", True, False, 1.0),
 ]
 
 
@@ -321,6 +328,10 @@ PACKED_CASES = [
     (513, 768, 32, 8, 384, None),
     (320, 256, 4, 2, 128, None),       # 160 rows per expert on average: deep pipeline (160-row passes)
     (322, 256, 4, 2, 128, None),       # 161 on average: default pipeline (192-row passes)
+    # K long enough for the unrolled main loops of both pipeline shapes (GEMM2 K = I)
+    (320, 768, 4, 2, 640, None),       # deep GEMM2 (nk 10), GEMM1 nk 12
+    (400, 1024, 4, 2, 1024, None),     # default GEMM2 and GEMM1, nk 16: the main loop twice
+    (1500, 512, 4, 2, 640, 0),         # one expert with 1,500 rows: 8 passes with cached weight loads
 ]
 
 

@@ -192,4 +192,16 @@ def test_layer_quantized_tokens_full_size_sampled(mode):
     err = max_rel_err(host(r["out"].float())[rows], want)
     log("  sampled out max_rel_err", err)
     assert err <= BF16_TOL
+    # whole segments of the first and the busiest expert (GEMM1 on the codes at
+    # K = 7168, every column tile), and the shared expert over every token (its
+    # GEMM1 runs on its own, its GEMM2 inside the routed GEMM2)
+    x = inputs.oracle_view(t["x"])
+    st, off, counts = host(r["sorted_token"]), host(r["offsets"]), host(r["counts"])
+    G.check_expert_segments(x, st, off, inputs.ExpertView(t["w_gate"]), inputs.ExpertView(t["w_up"]),
+                            inputs.ExpertView(t["w_down"]), [0, int(np.argmax(counts))], {mode: r["y_perm"]},
+                            BF16_TOL, quant=mode)
+    want_sh = O.swiglu_ffn(x, *(inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")))
+    err = max_rel_err(host(r["shared_out"].float()), want_sh)
+    log("  shared_out (all tokens) max_rel_err", err)
+    assert err <= BF16_TOL
     G.release_cached_weights()
