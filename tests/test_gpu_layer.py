@@ -159,8 +159,8 @@ MULTI_FORMS = {
     "packed_fused": dict(SMALL["dsv3_like_bf16"], d=512, I=256, I_shared=256, weight_layout="packed"),
     # packed weights, the shared expert as its own FFN on the second stream (I_shared != I)
     "packed_two_streams": dict(SMALL["dsv3_like_bf16"], d=512, I=256, I_shared=128, weight_layout="packed"),
-    # row-major weights (tiled GEMMs), the shared expert on the second stream
-    "rowmajor": dict(SMALL["dsv3_like_bf16"]),
+    # row-major weights (tiled GEMMs), the shared expert on the second stream (I_shared != I)
+    "rowmajor": dict(SMALL["dsv3_like_bf16"], d=512, I=256, I_shared=384),
 }
 
 
