@@ -300,19 +300,27 @@ def test_layer_full_size(name):
 def test_pending_hip_error_is_not_reported_by_the_next_call():
     """A HIP error left pending by unrelated earlier work on the thread (here an
     invalid device ordinal, rejected by the runtime on the host) is cleared by
-    the next library call instead of being reported as its failure."""
+    the next library call instead of being reported as its failure. Every
+    buffer and stream is made beforehand, so no other HIP call runs between
+    the failing one and the library call."""
     import ctypes
     import os
 
     # the HIP runtime the process already uses (torch's and the library's): no second copy is loaded
     hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_LAZY)
     p = SMALL["dsv3_like_bf16"]
+    cfg = G.moe_cfg(p)
     t = G.device_inputs(p, seed=8)
     ref = G.run_layer(p, t)
+    ws = moe.alloc_workspace(cfg, p["T"])
+    out = torch.full_like(ref["out"], float("nan"))
+    s_main, s_aux = torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     assert hip.hipSetDevice(ctypes.c_int(4096)) != 0      # leaves hipErrorInvalidDevice pending
-    r = G.run_layer(p, t)                                  # would raise MOE_ERR_HIP if it saw it
-    assert torch.equal(ref["out"], r["out"])
+    moe.moe_layer(cfg, p["T"], t["x"], t["w_router"], t["bias"], t["w_gate"], t["w_up"], t["w_down"],
+                  t["ws_gate"], t["ws_up"], t["ws_down"], out, ws, s_main=s_main, s_aux=s_aux)
+    torch.cuda.synchronize()
+    assert torch.equal(ref["out"], out)
 
 
 def test_layer_from_threads_that_exit():
