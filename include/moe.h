@@ -180,6 +180,25 @@ int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, in
                  int32_t* inv_perm, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * moe_dispatch_noalloc — moe_dispatch with no workspace argument, for callers
+ * that cannot allocate device memory or pass a workspace: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same arguments (minus ws, ws_bytes) and the same results as moe_dispatch.
+ * Its per-chunk expert masks and bases live in a device array owned by the
+ * library, one copy per GPU of 3 MiB, held until the process ends; the call
+ * finds its address on its first use on each device and allocates nothing.
+ * Limit: ceil(T / 64) * E <= 262144 (T <= 65536 tokens at E = 256); beyond it
+ * the call returns MOE_ERR_UNSUPPORTED and enqueues nothing. Nothing in the
+ * array needs to start at zero: a call writes every entry it reads. All calls
+ * on one GPU share that array: calls ordered on one stream are safe, calls
+ * that overlap in time on one GPU (several streams or threads) race and give
+ * undefined results.
+ */
+int moe_dispatch_noalloc(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, int32_t* counts,
+                         int32_t* offsets, int32_t* sorted_token, int32_t* sorted_assign, int32_t* inv_perm,
+                         hipStream_t stream);
+
+/*
  * moe_expert_ffn — the per-expert SwiGLU FFN over the dispatched rows
  * (App. M step 3 / App. F: GEMM1 gate+up, SwiGLU, GEMM2 down), as one grouped
  * GEMM pair: for every expert e and row r in [offsets[e], offsets[e+1]):

@@ -517,6 +517,41 @@ int moe_dispatch(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, in
   return e == hipSuccess ? MOE_OK : hip_fail(e, "dispatch");
 }
 
+int moe_dispatch_noalloc(const moe_config_t* cfg, int32_t T, const int32_t* topk_idx, int32_t* counts,
+                         int32_t* offsets, int32_t* sorted_token, int32_t* sorted_assign, int32_t* inv_perm,
+                         hipStream_t stream) {
+  MOE_CHECK(validate(cfg, T));
+  MOE_CHECK(need(topk_idx, "topk_idx"));
+  MOE_CHECK(need(counts, "counts"));
+  MOE_CHECK(need(offsets, "offsets"));
+  MOE_CHECK(need(sorted_token, "sorted_token"));
+  MOE_CHECK(need(inv_perm, "inv_perm"));
+  if (sorted_assign && !aligned16(sorted_assign)) return fail(MOE_ERR_INVALID_ARG, "sorted_assign is not 16-byte aligned");
+  const size_t items = (size_t)((T + moe::kDispatchChunk - 1) / moe::kDispatchChunk) * (size_t)cfg->E;
+  if (items > moe::kDispatchNoAllocItems)
+    return fail(MOE_ERR_UNSUPPORTED, "moe_dispatch_noalloc: ceil(T/64)*E = " + std::to_string(items) +
+                                         " exceeds its scratch limit of " + std::to_string(moe::kDispatchNoAllocItems));
+  if (T == 0) return MOE_OK;
+  clear_pending_error();
+  void* scr = nullptr;
+  hipError_t e = moe::dispatch_noalloc_scratch(&scr);
+  if (e != hipSuccess) return hip_fail(e, "dispatch scratch address");
+  moe::DispatchParams d{};
+  d.topk_idx = topk_idx;
+  d.T = T;
+  d.E = cfg->E;
+  d.k = cfg->k;
+  d.masks = static_cast<uint64_t*>(scr);
+  d.bases = reinterpret_cast<int32_t*>(static_cast<char*>(scr) + moe::kDispatchNoAllocItems * 8);
+  d.counts = counts;
+  d.offsets = offsets;
+  d.sorted_token = sorted_token;
+  d.sorted_assign = sorted_assign;
+  d.inv_perm = inv_perm;
+  e = moe::launch_dispatch(d, stream);
+  return e == hipSuccess ? MOE_OK : hip_fail(e, "dispatch");
+}
+
 int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int32_t* sorted_token,
                    const int32_t* offsets, const void* w_gate, const void* w_up, const void* w_down, void* y_perm,
                    void* ws, size_t ws_bytes, hipStream_t stream) {

@@ -21,6 +21,14 @@
 //                i.e. the number of earlier tokens that chose e.
 #include "moe_internal.h"
 
+#include <mutex>
+
+// Scratch of moe_dispatch_noalloc: the per-chunk masks and bases of a
+// dispatch whose caller passes no workspace. One copy per GPU, held until
+// the process ends. In host code this name is only a stand-in for the
+// symbol: the device address comes from hipGetSymbolAddress (per device).
+static __device__ __align__(256) unsigned char scratch[moe::kDispatchNoAllocBytes];
+
 namespace moe {
 namespace {
 
@@ -173,6 +181,24 @@ __global__ void __launch_bounds__(64 * kWaves) dispatch_scatter_kernel(DispatchP
 }
 
 }  // namespace
+
+hipError_t dispatch_noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  static std::mutex mu;
+  static void* addr[64] = {};
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* a = nullptr;
+    if ((e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!a) return hipErrorInvalidSymbol;
+    addr[dev] = a;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_dispatch(const DispatchParams& p, hipStream_t s) {
   const int nchunks = (p.T + kDispatchChunk - 1) / kDispatchChunk;

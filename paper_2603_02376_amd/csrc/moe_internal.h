@@ -129,6 +129,14 @@ struct DispatchParams {
   int32_t n_zero;
 };
 hipError_t launch_dispatch(const DispatchParams& p, hipStream_t s);
+// Library-owned dispatch scratch (moe_dispatch_noalloc): room for the masks
+// and bases of ceil(T / kDispatchChunk) * E <= kDispatchNoAllocItems items
+// (masks first, then the bases at byte kDispatchNoAllocItems * 8).
+constexpr size_t kDispatchNoAllocItems = 262144;
+constexpr size_t kDispatchNoAllocBytes = kDispatchNoAllocItems * (8 + 4);
+// Device address of this device's copy of that scratch (looked up once per
+// device with hipGetSymbolAddress, then cached; allocates nothing).
+hipError_t dispatch_noalloc_scratch(void** out);
 
 struct CombineParams {
   const void* y_perm;      // [T*k][d]

@@ -61,6 +61,7 @@ _SIGS = {
     "moe_workspace_size": (_SZ, [_CFG, _I32]),
     "moe_route": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_dispatch": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    "moe_dispatch_noalloc": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "moe_expert_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_shared_ffn": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     "moe_quantize": (ctypes.c_int, [_CFG, _I32, _VP, _VP, _VP, _VP]),
@@ -211,6 +212,19 @@ def moe_dispatch(cfg: MoeConfig, T, topk_idx, counts, offsets, sorted_token, sor
                               _ptr(sorted_assign, "sorted_assign", torch.int32, n),
                               _ptr(inv_perm, "inv_perm", torch.int32, n),
                               _ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_dispatch_noalloc(cfg: MoeConfig, T, topk_idx, counts, offsets, sorted_token, sorted_assign, inv_perm,
+                         stream=None):
+    """moe_dispatch with the library's own scratch (no workspace argument)."""
+    c = cfg.c()
+    n = T * cfg.k
+    _check(lib().moe_dispatch_noalloc(ctypes.byref(c), T, _ptr(topk_idx, "topk_idx", torch.int32, n),
+                                      _ptr(counts, "counts", torch.int32, cfg.E),
+                                      _ptr(offsets, "offsets", torch.int32, cfg.E + 1),
+                                      _ptr(sorted_token, "sorted_token", torch.int32, n),
+                                      _ptr(sorted_assign, "sorted_assign", torch.int32, n),
+                                      _ptr(inv_perm, "inv_perm", torch.int32, n), _stream(stream)))
 
 
 def moe_expert_ffn(cfg: MoeConfig, T, x, sorted_token, offsets, w_gate, w_up, w_down, y_perm, ws, stream=None):
