@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmoe.so")
 
-SOURCES = ["gemm_bf16.hip", "gemm_stream.hip", "gemm_f32.hip", "route.hip", "dispatch.hip", "combine.hip", "quant.hip", "ep.hip", "api.cpp"]
+SOURCES = ["gemm_bf16.hip", "gemm_stream.hip", "gemm_dense.hip", "gemm_f32.hip", "route.hip", "dispatch.hip", "combine.hip", "quant.hip", "ep.hip", "api.cpp"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

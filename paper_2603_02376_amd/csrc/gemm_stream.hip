@@ -668,6 +668,8 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
 
 hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
   if ((p.M <= 0 && p.x_rows <= 0) || p.N <= 0) return hipSuccess;
+  // groups of many rows are bound by the matrix cores, not by the weight stream
+  if (gemm_dense_eligible(p)) return launch_gemm_dense(p, epi, s);
   if (p.a_scale) {
     if (epi != EPI_SWIGLU) return hipErrorInvalidValue;
     return p.a_fp8 ? launch_stream<EPI_SWIGLU, true, true>(p, s) : launch_stream<EPI_SWIGLU, true>(p, s);

@@ -85,6 +85,13 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, int epilogue, bool out_f32, hi
 // Weight-streaming bf16 grouped GEMM over packed weights (B0 = packed buffer;
 // N % 128 == 0 for EPI_SWIGLU, N % 256 == 0 for EPI_STORE, K % 64 == 0).
 hipError_t launch_gemm_stream(const GemmProblem& p, int epilogue, hipStream_t s);
+// Compute-bound grouped GEMM over the same packed weights (gemm_dense.hip):
+// 256x256 tiles with both operands shared through LDS, for groups of many
+// rows (average >= 512 per group, at most 256 groups), no extra group, no
+// quantized tokens, no row segments or workgroup cap, K % 128 == 0 and
+// K >= 256. launch_gemm_stream hands eligible problems to it.
+bool gemm_dense_eligible(const GemmProblem& p);
+hipError_t launch_gemm_dense(const GemmProblem& p, int epilogue, hipStream_t s);
 // Zeroes n queue heads of launch_gemm_stream (a one-workgroup kernel, so
 // it can be captured in a graph).
 hipError_t launch_queue_reset(int32_t* q, int n, hipStream_t s);

@@ -242,7 +242,8 @@ def test_shared_ffn(T, d, Is, dtype):
     assert max_rel_err(host(out.float()), want) <= (BF16_TOL if dtype == "bf16" else F32_TOL)
 
 
-@pytest.mark.parametrize("T,d,Is", [(300, 512, 256), (5, 256, 128), (700, 256, 384)])
+@pytest.mark.parametrize("T,d,Is", [(300, 512, 256), (5, 256, 128), (700, 256, 384),
+                                    (513, 256, 128), (1030, 512, 256)])   # from 512 rows: the compute-bound kernel
 def test_shared_ffn_packed(T, d, Is):
     log("shared_ffn packed", T, d, Is)
     p = dict(T=T, d=d, E=1, k=1, I=128, dtype="bf16", n_shared=1, I_shared=Is, bias="none")
@@ -335,7 +336,19 @@ PACKED_CASES = [
 ]
 
 
-@pytest.mark.parametrize("case", PACKED_CASES, ids=lambda c: "T{}_d{}_E{}_k{}_I{}".format(*c[:5]))
+# Groups averaging >= 512 rows take the compute-bound kernel (256-row blocks
+# plus a remainder block, 256x256 tiles through an LDS ring).
+DENSE_CASES = [
+    (1024, 256, 2, 1, 128, None),      # 512 rows per expert: two full blocks; one column tile; K 256 and 128
+    (2100, 512, 4, 2, 1152, None),     # ~1,050 rows: four full blocks + a remainder; 9 GEMM1 column tiles
+    (1300, 768, 2, 1, 256, None),      # ~650 rows: two blocks + a remainder; GEMM1 K 768
+    (600, 256, 1, 1, 128, None),       # one expert of 600 rows (88-row remainder: one wave row idle)
+    (2049, 256, 4, 1, 128, 0),         # every token to expert 0: eight full blocks + one row; three empty experts
+    (1540, 512, 3, 1, 640, None),      # ~513 rows: remainders of a few rows; GEMM2 K 640
+]
+
+
+@pytest.mark.parametrize("case", PACKED_CASES + DENSE_CASES, ids=lambda c: "T{}_d{}_E{}_k{}_I{}".format(*c[:5]))
 def test_expert_ffn_packed(case):
     T, d, E, k, I, hot = case
     log("expert_ffn packed", case)
