@@ -415,6 +415,7 @@ hipError_t launch_dense(const GemmProblem& p, hipStream_t s) {
   const long long upper = blocks_upper * (p.N / tcols);
   if (upper <= 0) return hipSuccess;
   long long grid = device_cu_count();
+  if (p.max_wg > 0 && grid > p.max_wg) grid = p.max_wg;
   if (grid > upper) grid = upper;
   if (grid >= 8) grid -= grid % 8;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), kRing, s, p);
@@ -424,7 +425,7 @@ hipError_t launch_dense(const GemmProblem& p, hipStream_t s) {
 }  // namespace
 
 bool gemm_dense_eligible(const GemmProblem& p) {
-  if (p.a_scale || p.x_rows != 0 || p.seg_end || p.max_wg != 0) return false;
+  if (p.a_scale || p.x_rows != 0 || p.seg_end) return false;
   if (p.K % 128 != 0 || p.K < 256) return false;
   if ((size_t)p.a_rows * (size_t)p.K * 2 > 0xFFFFFFFFull || (size_t)(p.K / 64) * 32768 > 0x7FFFFFFFull) return false;
   const int groups = p.offsets ? p.groups : 1;

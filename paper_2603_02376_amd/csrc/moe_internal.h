@@ -88,8 +88,8 @@ hipError_t launch_gemm_stream(const GemmProblem& p, int epilogue, hipStream_t s)
 // Compute-bound grouped GEMM over the same packed weights (gemm_dense.hip):
 // 256x256 tiles with both operands shared through LDS, for groups of many
 // rows (average >= 512 per group, at most 256 groups), no extra group, no
-// quantized tokens, no row segments or workgroup cap, K % 128 == 0 and
-// K >= 256. launch_gemm_stream hands eligible problems to it.
+// quantized tokens, no row segments, K % 128 == 0 and K >= 256 (max_wg caps
+// its grid too). launch_gemm_stream hands eligible problems to it.
 bool gemm_dense_eligible(const GemmProblem& p);
 hipError_t launch_gemm_dense(const GemmProblem& p, int epilogue, hipStream_t s);
 // Zeroes n queue heads of launch_gemm_stream (a one-workgroup kernel, so
