@@ -83,7 +83,7 @@ def measured_traffic(workload: str, layout: str):
     return rec.get("bytes_per_call")
 
 
-CPU_EXPERTS = 64  # whole experts the CPU baseline runs; the rest of the expert FFN is scaled from them
+CPU_EXPERTS = 0  # whole experts the CPU baseline runs (0: every touched expert, i.e. the whole layer)
 EP_LINK_WORKGROUPS = 16  # workgroups of the emulated exchange (~77 GB/s measured: about one xGMI link, one way)
 EP_CHUNKS = (4, 8, 16)
 
@@ -402,7 +402,7 @@ def run_workload(name: str, steps: int, warmup: int, want_cpu: bool, cpu_experts
         multilayer_ms_per_layer=ml,
     )
     if want_cpu:
-        log(f"[bench] {name}: CPU oracle baseline ({cpu_experts} whole experts, all tokens routed)")
+        log(f"[bench] {name}: CPU oracle baseline ({cpu_experts or 'all'} whole experts, all tokens routed)")
         res["cpu"] = cpu_baseline(p, t, cpu_experts)
     del t, ws, out, y, w_ffn, w_sh
     torch.cuda.empty_cache()
@@ -433,7 +433,8 @@ def cpu_baseline(p, t, n_experts: int = CPU_EXPERTS):
     # the sampled experts: routed once before the clock starts, their weights copied to host RAM
     touched = np.nonzero(O.dispatch(O.route(O.gate_logits(x, wr), **kw)[0], E)[0])[0]
     rng = np.random.default_rng(0)
-    chosen = np.sort(rng.choice(touched, min(n_experts, touched.size), replace=False))
+    n_pick = touched.size if n_experts <= 0 else min(n_experts, touched.size)
+    chosen = np.sort(rng.choice(touched, n_pick, replace=False))
     host_w = {n: {int(e): inputs.oracle_view(t[n][int(e)]) for e in chosen} for n in ("w_gate", "w_up", "w_down")}
     sh = [inputs.oracle_view(t[n]) for n in ("ws_gate", "ws_up", "ws_down")] if p["n_shared"] else None
 
@@ -465,10 +466,13 @@ def cpu_baseline(p, t, n_experts: int = CPU_EXPERTS):
     return dict(value=T / est, unit="tokens/s", cores=threads or len(os.sched_getaffinity(0)),
                 host_cpus=len(os.sched_getaffinity(0)), blas=blas, kind="oracle", seconds_timed=t3 - t0,
                 seconds_layer_estimate=est,
-                sample=f"the {p.get('name')} workload (T={T}): gate, routing, dispatch and combine of all {T} tokens"
-                       f"{', the shared expert on all of them' if sh else ''}, and the SwiGLU FFN of every row of "
-                       f"{len(chosen)} of the {n_touched} touched experts (seeded choice), in fp64; the expert-FFN "
-                       f"time scaled by {n_touched}/{len(chosen)} to the whole layer")
+                sample=(f"the whole {p.get('name')} layer (T={T}): gate, routing, dispatch, the SwiGLU FFN of all "
+                        f"{n_touched} touched experts{', the shared expert' if sh else ''} and the combine of all {T} "
+                        f"tokens, in fp64" if len(chosen) == n_touched else
+                        f"the {p.get('name')} workload (T={T}): gate, routing, dispatch and combine of all {T} tokens"
+                        f"{', the shared expert on all of them' if sh else ''}, and the SwiGLU FFN of every row of "
+                        f"{len(chosen)} of the {n_touched} touched experts (seeded choice), in fp64; the expert-FFN "
+                        f"time scaled by {n_touched}/{len(chosen)} to the whole layer"))
 
 
 def main():
@@ -482,7 +486,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the side measurements (other workloads, multi-layer)")
     ap.add_argument("--cpu-experts", type=int, default=CPU_EXPERTS,
-                    help="whole experts the CPU-oracle baseline runs (the rest of its expert FFN is scaled)")
+                    help="whole experts the CPU-oracle baseline runs, the rest of its expert FFN scaled (0: all)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run 3 plain device copies of this many MiB (reference for HBM byte counters)")
     ap.add_argument("--ffn-only", action="store_true",
