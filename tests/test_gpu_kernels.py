@@ -345,6 +345,10 @@ DENSE_CASES = [
     (600, 256, 1, 1, 128, None),       # one expert of 600 rows (88-row remainder: one wave row idle)
     (2049, 256, 4, 1, 128, 0),         # every token to expert 0: eight full blocks + one row; three empty experts
     (1540, 512, 3, 1, 640, None),      # ~513 rows: remainders of a few rows; GEMM2 K 640
+    # skewed (average below 512 rows, so the weight stream): one hot expert among small ones
+    (1200, 512, 16, 2, 256, 0),        # one expert of 1,200 rows (7 passes), fifteen of ~80
+    (700, 768, 32, 4, 384, 5),         # one of 700 rows (GEMM2 K 384), the others ~68
+    (512, 256, 8, 2, 256, 3),          # one of 512 rows
 ]
 
 
