@@ -58,7 +58,7 @@ def algorithmic(p: dict, counts) -> dict:
                 layer_flops=layer_flops, bytes_per_expert=w_expert)
 
 
-GEMM_SOURCES = {"packed": ("gemm_stream.hip",), "rowmajor": ("gemm_bf16.hip",)}
+GEMM_SOURCES = {"packed": ("gemm_stream.hip", "gemm_dense.hip"), "rowmajor": ("gemm_bf16.hip",)}
 
 
 def kernel_source_hash(layout: str = "packed") -> str:
