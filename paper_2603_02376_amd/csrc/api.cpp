@@ -270,11 +270,14 @@ struct FusedShared {
 // x_scales: x holds int8 codes of rows with these fp32 scales (packed only).
 // seg_end, max_wg (packed only): group g owns rows [offsets[g], seg_end[g]);
 // at most max_wg workgroups per GEMM (0: one per compute unit).
+// rows_exact: the groups hold exactly `rows` rows between them (false for a
+// range of groups or row segments: the GEMMs then keep the weight-streaming
+// kernel, whose choice does not depend on the groups' sizes).
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
                    int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
-                   int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false) {
+                   int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false, bool rows_exact = true) {
   if (packed && queues && !queues_zeroed) {
     const hipError_t e = moe::launch_queue_reset(queues, 16, s);
     if (e != hipSuccess) return e;
@@ -303,6 +306,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   up.a_fp8 = x_fp8 ? 1 : 0;
   up.seg_end = seg_end;
   up.max_wg = max_wg;
+  up.rows_exact = rows_exact && !seg_end ? 1 : 0;
   hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
   if (e != hipSuccess) return e;
   moe::GemmProblem down{};
@@ -325,6 +329,7 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   down.tile_queue = queues ? queues + 8 : nullptr;
   down.seg_end = seg_end;
   down.max_wg = max_wg;
+  down.rows_exact = up.rows_exact;
   return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
@@ -429,7 +434,7 @@ hipError_t run_ffn_segments(const moe_config_t& c, int32_t n_rows, const void* x
   const char* wd = static_cast<const char*>(w_down) + (size_t)e0 * c.d * c.I * 2;
   return run_ffn(c, n_rows, n_rows, e1 - e0, c.I, x, nullptr, seg_begin + e0, wgu, nullptr, wd, ws + L.h, y, s, true,
                  nullptr, reinterpret_cast<int32_t*>(ws + L.queues), nullptr, seg_end ? seg_end + e0 : nullptr,
-                 max_wg);
+                 max_wg, false, false, /*rows_exact=*/false);
 }
 
 hipError_t run_ep_copy(const moe_config_t& c, int32_t mode, int32_t n_rows, const void* src, int32_t src_tokens,

@@ -425,7 +425,7 @@ hipError_t launch_dense(const GemmProblem& p, hipStream_t s) {
 }  // namespace
 
 bool gemm_dense_eligible(const GemmProblem& p) {
-  if (p.a_scale || p.x_rows != 0 || p.seg_end) return false;
+  if (p.a_scale || p.x_rows != 0 || p.seg_end || (p.offsets && !p.rows_exact)) return false;
   if (p.K % 128 != 0 || p.K < 256) return false;
   if ((size_t)p.a_rows * (size_t)p.K * 2 > 0xFFFFFFFFull || (size_t)(p.K / 64) * 32768 > 0x7FFFFFFFull) return false;
   const int groups = p.offsets ? p.groups : 1;

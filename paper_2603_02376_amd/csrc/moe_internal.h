@@ -74,6 +74,10 @@ struct GemmProblem {
   // instead of [offsets[g], offsets[g+1]) (nullptr: adjacent segments), so a
   // call can cover part of every group's rows.
   const int32_t* seg_end;
+  // 1: the groups' segments hold exactly M rows between them (a call over
+  // every group of a dispatch), so M / groups is their average size; 0: M
+  // only bounds them (a range of groups, or row segments).
+  int32_t rows_exact;
   // Weight-streaming kernel only: at most this many workgroups (0: one per
   // compute unit), leaving compute units to kernels on other streams.
   int32_t max_wg;
@@ -87,9 +91,10 @@ hipError_t launch_gemm_bf16(const GemmProblem& p, int epilogue, bool out_f32, hi
 hipError_t launch_gemm_stream(const GemmProblem& p, int epilogue, hipStream_t s);
 // Compute-bound grouped GEMM over the same packed weights (gemm_dense.hip):
 // 256x256 tiles with both operands shared through LDS, for groups of many
-// rows (average >= 512 per group, at most 256 groups), no extra group, no
-// quantized tokens, no row segments, K % 128 == 0 and K >= 256 (max_wg caps
-// its grid too). launch_gemm_stream hands eligible problems to it.
+// rows (M exact, rows_exact, and an average >= 512 per group, at most 256
+// groups), no extra group, no quantized tokens, no row segments, K % 128 == 0
+// and K >= 256 (max_wg caps its grid too). launch_gemm_stream hands eligible
+// problems to it.
 bool gemm_dense_eligible(const GemmProblem& p);
 hipError_t launch_gemm_dense(const GemmProblem& p, int epilogue, hipStream_t s);
 // Zeroes n queue heads of launch_gemm_stream (a one-workgroup kernel, so
