@@ -413,7 +413,8 @@ def cpu_baseline(p, t, n_experts: int = CPU_EXPERTS):
     """The oracle, as it stands, timed on the host cores over the whole
     workload's routing and a seeded subset of whole experts: gate logits and
     routing of all T tokens, dispatch, the SwiGLU FFN of every row of
-    n_experts of the touched experts (a seeded choice), the shared expert on
+    n_experts of the touched experts (a seeded choice; n_experts <= 0: every
+    touched expert, the whole layer, the default), the shared expert on
     all T tokens, and the combine of all tokens, everything in fp64. The
     expert-FFN time is scaled by touched / n_experts (every touched expert of
     a uniformly routed workload has about the same rows); the rest is timed

@@ -9,10 +9,11 @@
 //
 //   * Output tiles of 256 token rows x 256 weight columns (GEMM1: 128 h
 //     columns with their gate and up rows; GEMM2: 256 output columns), one
-//     workgroup of 4 waves per compute unit, each wave a 128 x 128 quarter
-//     (16 accumulator tiles of 32x32 in AGPRs). A K step of 32 feeds every
-//     wave 32 MFMAs (v_mfma_f32_32x32x16_bf16) from 16 fragment reads: the
-//     largest register tile per wave, hence the fewest LDS bytes per FLOP.
+//     workgroup of 8 waves per compute unit (two per SIMD, so one wave's LDS
+//     and barrier waits are covered by the other's MFMAs), each wave 128
+//     token rows x 64 weight columns (8 accumulator tiles of 32x32 in
+//     AGPRs). A K step of 32 feeds every wave 16 MFMAs
+//     (v_mfma_f32_32x32x16_bf16) from 12 fragment reads.
 //   * Both operands go through a 4-slot LDS ring of 32 KB (16 KB of token
 //     rows, 16 KB of weights per step) filled by direct global->LDS loads
 //     (buffer_load_dwordx4 ... lds): no register staging, loads issued three
