@@ -87,9 +87,11 @@ __device__ __forceinline__ void with_count(int n, F&& f) {
 }
 
 // Token-row region of a slot: 64-byte rows, 16-byte chunk c of row r at
-// chunk c ^ ((r >> 1) & 3), so the 16 rows a quarter-wave reads at one
-// logical chunk fall on distinct bank groups.
-__device__ __forceinline__ int a_off(int row, int chunk) { return (row << 6) + ((chunk ^ ((row >> 1) & 3)) << 4); }
+// chunk c ^ ((r >> 2) & 3). The LDS serves a 16-byte read 16 lanes at a
+// time from a 256-byte window of banks; the 16 consecutive rows those lanes
+// read at one logical chunk then fall on 16 distinct 16-byte bank groups
+// (4 (r % 4) + physical chunk).
+__device__ __forceinline__ int a_off(int row, int chunk) { return (row << 6) + ((chunk ^ ((row >> 2) & 3)) << 4); }
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 __device__ __forceinline__ int block_scan(int v, int* scratch, int* total) {
@@ -173,7 +175,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
 
   // this lane's part of a token-row direct load: row (lane >> 2) of a 16-row
   // group, fetching logical chunk lc so that it lands at physical chunk lane & 3
-  const int lc = (lane & 3) ^ ((lane >> 3) & 3);
+  const int lc = (lane & 3) ^ ((lane >> 4) & 3);
 
   for (int tile = vb; tile < total_tiles; tile += G) {
     // ---- decode: group e, m-block mb, column tile nt
