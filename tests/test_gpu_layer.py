@@ -283,6 +283,15 @@ def test_layer_full_size(name):
             err = max_rel_err(G.host(res[lay]["shared_out"].float()), want_sh)
             G.log(f"  shared_out ({lay}, all {p0['T']} tokens): max_rel_err {err:.3e}")
             assert err <= tol
+        # the shared expert on its own (packed: one group of T rows, the
+        # compute-bound GEMMs from 512 rows) gives the fused layer's bits
+        cfg = G.moe_cfg(dict(p0, weight_layout="packed"))
+        sg, sd = moe.pack_shared_weights(cfg, t["ws_gate"], t["ws_up"], t["ws_down"])
+        alone = torch.full_like(b["shared_out"], float("nan"))
+        moe.moe_shared_ffn(cfg, p0["T"], t["x"], sg, None, sd, alone, moe.alloc_workspace(cfg, p0["T"]))
+        torch.cuda.synchronize()
+        assert torch.equal(alone, b["shared_out"]), "moe_shared_ffn differs from the fused shared expert"
+        del sg, sd, alone
     rng = np.random.default_rng(0)
     rows = np.unique(np.concatenate([[0, p0["T"] - 1], rng.choice(p0["T"], SAMPLE, replace=False)]))
     routing = G.check_routing_and_dispatch_exact(p0, t, b)
