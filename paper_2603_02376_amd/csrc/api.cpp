@@ -67,7 +67,7 @@ constexpr int kQueueInts = 32;
 // Byte offsets of every scratch region inside the caller's workspace.
 struct Layout {
   size_t gate_partials, logits, topk_idx, topk_w, masks, bases, counts, offsets, sorted_token, sorted_assign,
-      inv_perm, h, y_perm, shared_h, shared_out, queues, qcodes, qscales, total;
+      inv_perm, h, y_perm, shared_h, shared_out, queues, qcodes, qscales, dense_part, dense_part_bytes, total;
 };
 
 Layout make_layout(const moe_config_t& c, int32_t T) {
@@ -100,6 +100,8 @@ Layout make_layout(const moe_config_t& c, int32_t T) {
   const bool q8 = c.token_quant != MOE_QUANT_NONE;
   L.qcodes = take(q8 ? t * c.d : 0);  // moe_layer's quantized tokens
   L.qscales = take(q8 ? t * 4 : 0);
+  L.dense_part_bytes = c.weight_layout == MOE_LAYOUT_PACKED ? moe::dense_part_bytes((int64_t)tk, c.E, c.d, c.I) : 0;
+  L.dense_part = take(L.dense_part_bytes);
   L.total = off;
   return L;
 }
@@ -273,11 +275,14 @@ struct FusedShared {
 // rows_exact: the groups hold exactly `rows` rows between them (false for a
 // range of groups or row segments: the GEMMs then keep the weight-streaming
 // kernel, whose choice does not depend on the groups' sizes).
+// dense_part: workspace in which the compute-bound GEMM2 may split the K
+// range of short remainder blocks (nullptr: never).
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
                    int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
-                   int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false, bool rows_exact = true) {
+                   int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false, bool rows_exact = true,
+                   void* dense_part = nullptr, size_t dense_part_bytes = 0) {
   if (packed && queues && !queues_zeroed) {
     const hipError_t e = moe::launch_queue_reset(queues, 16, s);
     if (e != hipSuccess) return e;
@@ -330,6 +335,8 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   down.seg_end = seg_end;
   down.max_wg = max_wg;
   down.rows_exact = up.rows_exact;
+  down.dense_part = dense_part;
+  down.dense_part_bytes = (int64_t)dense_part_bytes;
   return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
@@ -575,7 +582,8 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
                                static_cast<char*>(ws) + L.h, y_perm, stream, packed, nullptr,
-                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues));
+                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), nullptr, nullptr, 0,
+                               false, false, true, static_cast<char*>(ws) + L.dense_part, L.dense_part_bytes);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
 }
 
@@ -759,7 +767,8 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   }
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
                    w_down, w + L.h, y, s_main, packed, (fuse || fuse_down) ? &fs : nullptr, queues,
-                   q8 ? qscales : nullptr, nullptr, 0, f8, /*queues_zeroed=*/true)) !=
+                   q8 ? qscales : nullptr, nullptr, 0, f8, /*queues_zeroed=*/true, /*rows_exact=*/true,
+                   w + L.dense_part, L.dense_part_bytes)) !=
       hipSuccess)
     return hip_fail(e, "expert FFN");
   if (own) {

@@ -66,6 +66,20 @@ constexpr int kStreamStore = 19;               // output stores: sc0 sc1 nt
 // is the bound and gemm_stream is used).
 constexpr int kDenseMinAvgRows = 512;
 
+// K split of the short remainder blocks of GEMM2. A remainder block of at
+// most 192 rows streams a column tile's whole K range of weights for a few
+// rows; with a long K (Mixtral: 14336, two rounds of full 256-row tiles of
+// ~365 us each) the remainder tiles make a third round on a quarter of the
+// compute units. Each such tile is cut into kPartKs tiles over consecutive
+// quarters of K that write fp32 partial sums (up to kPartRows rows x 256
+// columns each) to a workspace; dense_part_reduce_kernel then adds the
+// quarters in order (a fixed order: the result does not depend on which
+// workgroup ran which quarter when) and writes the bf16 rows.
+constexpr int kPartKs = 4;
+constexpr int kPartRows = 192;                 // rows of a section-2 (remainder) block, at most
+constexpr int kPartMetaBytes = 4096;           // [0]: remainder blocks, [1 + i]: group of block i
+constexpr size_t kPartBudget = (size_t)256 << 20;
+
 template <typename F, int... Is>
 __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
   (f(std::integral_constant<int, Is>{}), ...);
@@ -168,8 +182,15 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
   }
   const int Nt = p.N / TCOLS;
   const int tiles1 = tstart[groups] * Nt;
-  const int total_tiles = tiles1 + n_rgroup * Nt;
+  // K parts of a section-2 tile (GEMM2 with a split workspace; nk % (4 KS) == 0, checked at launch)
+  const int KS = (EPI == EPI_STORE && p.part_ks > 1) ? p.part_ks : 1;
+  const int total_tiles = tiles1 + n_rgroup * Nt * KS;
   const int K = p.K, nk = K / kBK;  // nk % 4 == 0 (checked at launch)
+  if (KS > 1 && blockIdx.x == 0) {  // the remainder blocks, for dense_part_reduce_kernel
+    int32_t* const meta = static_cast<int32_t*>(p.dense_part);
+    if (tid == 0) meta[0] = n_rgroup;
+    if (tid < n_rgroup) meta[1 + tid] = rgroup[tid];
+  }
   const int G = gridDim.x, b = blockIdx.x;
   const int vb = (G % 8 == 0) ? (b % 8) * (G / 8) + (b / 8) : b;
 
@@ -178,8 +199,9 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
   const int lc = (lane & 3) ^ ((lane >> 4) & 3);
 
   for (int tile = vb; tile < total_tiles; tile += G) {
-    // ---- decode: group e, m-block mb, column tile nt
-    int e, mb, nt;
+    // ---- decode: group e, m-block mb, column tile nt (split: remainder block
+    // ridx's K part `part`)
+    int e, mb, nt, part = 0, ridx = 0;
     if (tile < tiles1) {
       const int q = tile / Nt;
       int lo = 0, hi = groups - 1;
@@ -198,14 +220,19 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
       nt = ntg * kNtGroup + rem % gsz;
     } else {
       const int t2 = tile - tiles1;
-      e = rgroup[t2 / Nt];
-      nt = t2 % Nt;
+      part = t2 % KS;  // the K parts of one (block, column tile) are adjacent
+      ridx = t2 / KS;
+      e = rgroup[ridx / Nt];
+      nt = ridx % Nt;
       mb = group_rows(e) / kBM;
     }
     const int gbeg = p.offsets ? min(max(p.offsets[e], 0), p.M) : 0;
     const int gend = p.offsets ? min(max(p.offsets[e + 1], gbeg), p.M) : p.M;
     const int row0 = gbeg + mb * kBM;
     const int rows = min(kBM, gend - row0);
+    const bool split = KS > 1 && tile >= tiles1;
+    const int nkl = split ? nk / KS : nk;  // K steps of this tile, from step kx0
+    const int kx0 = part * nkl;
 
     // token rows of this wave's direct loads (rows past the block re-read
     // its last row: a fixed count of loads per step, never stored)
@@ -232,12 +259,12 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
     // the 64-wide block x / 2, K slices 2 (x % 2) and 2 (x % 2) + 1.
     auto load_a = [&](int x, int s, int i) __attribute__((always_inline)) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rs, (lds_ptr_t)(smem + s * kSlotBytes + (i * 128 + wave * 16) * 64), 16,
-                                               (int)a_voff[i], x * 64, 0, 0);
+                                               (int)a_voff[i], (kx0 + x) * 64, 0, 0);
     };
     auto load_b = [&](int x, int s, int n) __attribute__((always_inline)) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           b_rs, (lds_ptr_t)(smem + s * kSlotBytes + kABytes + (wave * 2 + n) * 1024), 16, (int)(b_voff + n * 1024),
-          (x >> 1) * 32768 + (x & 1) * 4096, 0, 0);
+          ((kx0 + x) >> 1) * 32768 + ((kx0 + x) & 1) * 4096, 0, 0);
     };
 
     f32x16 acc[4][2];
@@ -328,7 +355,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
       asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(LOADS) : "memory");
       if constexpr (NACT > 0) read_frags(0, 0, 0);
       int x = 0;
-      for (; x + 4 < nk; x += 4)
+      for (; x + 4 < nkl; x += 4)
         static_for<4>([&](auto u_c) { step(x + u_c, u_c, T_{}, T_{}, W2{}); });
       step(x, std::integral_constant<int, 0>{}, T_{}, T_{}, W2{});
       step(x + 1, std::integral_constant<int, 1>{}, F_{}, T_{}, W1{});
@@ -341,6 +368,29 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
       with_count<2>(min(nact, 2), [&](auto n_c) { kloop(n_c, std::integral_constant<int, 1>{}); });
     }
 
+    if (split) {
+      // fp32 partial sums of K part `part`: row r, output column c at
+      // [(ridx KS + part) kPartRows + r] 256 + c (same register layout as below)
+      float* const dst = reinterpret_cast<float*>(static_cast<char*>(p.dense_part) + kPartMetaBytes) +
+                         ((size_t)ridx * KS + part) * (kPartRows * 256);
+      const int h = lane >> 5;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i < nact) {
+          const int r = (wm + 2 * i) * 32 + (lane & 31);  // < kPartRows: at most 6 fragments
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              f32x4 v;
+#pragma unroll
+              for (int c = 0; c < 4; ++c) v[c] = acc[i][j][4 * g + c];
+              *reinterpret_cast<f32x4*>(dst + (size_t)r * 256 + wn * 64 + j * 32 + 8 * g + 4 * h) = v;
+            }
+        }
+      }
+      continue;
+    }
     // ---- epilogue. acc[i][j] is the transposed 32x32 tile (weights were the
     // first MFMA operand): lane l holds token row (wm + 2 i) * 32 + l % 32 and
     // weight columns 8 g + 4 (l / 32) + 0..3 of fragment j in registers
@@ -403,6 +453,34 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
   }
 }
 
+// Adds the kPartKs fp32 partial sums of every split remainder block in K
+// order and writes its bf16 rows: one workgroup per (remainder block, column
+// tile), one output column per thread.
+__global__ void __launch_bounds__(256) dense_part_reduce_kernel(GemmProblem p) {
+  const int Nt = p.N / 256;
+  const int32_t* const meta = static_cast<const int32_t*>(p.dense_part);
+  const int i = blockIdx.x / Nt, nt = blockIdx.x % Nt;
+  if (i >= meta[0]) return;
+  const int e = min(max(meta[1 + i], 0), p.groups - 1);
+  const int gbeg = min(max(p.offsets[e], 0), p.M);
+  const int gend = min(max(p.offsets[e + 1], gbeg), p.M);
+  const int full = (gend - gbeg) / kBM * kBM;
+  const int row0 = gbeg + full, rows = min(gend - gbeg - full, kPartRows);
+  const float* const src = reinterpret_cast<const float*>(static_cast<const char*>(p.dense_part) + kPartMetaBytes) +
+                           (size_t)(i * Nt + nt) * kPartKs * (kPartRows * 256);
+  __bf16* const dst = static_cast<__bf16*>(p.C) + (size_t)nt * 256 + threadIdx.x;
+  for (int r = 0; r < rows; ++r) {
+    float acc = 0.f;
+#pragma unroll
+    for (int q = 0; q < kPartKs; ++q) acc += src[((size_t)q * kPartRows + r) * 256 + threadIdx.x];
+    dst[(size_t)(row0 + r) * p.ldc] = static_cast<__bf16>(acc);
+  }
+}
+
+size_t part_need(int groups, int nt) {
+  return (size_t)kPartMetaBytes + (size_t)groups * nt * kPartKs * kPartRows * 256 * 4;
+}
+
 template <int EPI>
 hipError_t launch_dense(const GemmProblem& p, hipStream_t s) {
   auto kern = gemm_dense_kernel<EPI>;
@@ -414,18 +492,34 @@ hipError_t launch_dense(const GemmProblem& p, hipStream_t s) {
   if (init_err != hipSuccess) return init_err;
   const int tcols = (EPI == EPI_SWIGLU) ? 128 : 256;
   const int groups = p.offsets ? p.groups : 1;
-  const long long blocks_upper = (p.M + kBM - 1) / kBM + (p.offsets ? groups : 0);
+  GemmProblem q = p;
+  q.part_ks = 1;
+  if (EPI == EPI_STORE && p.offsets && p.dense_part) {
+    const int nk = p.K / kBK;
+    if (nk % (4 * kPartKs) == 0 && nk >= 256 && (size_t)p.dense_part_bytes >= part_need(groups, p.N / 256))
+      q.part_ks = kPartKs;
+  }
+  const long long blocks_upper = (p.M + kBM - 1) / kBM + (p.offsets ? (long long)groups * q.part_ks : 0);
   const long long upper = blocks_upper * (p.N / tcols);
   if (upper <= 0) return hipSuccess;
   long long grid = device_cu_count();
   if (p.max_wg > 0 && grid > p.max_wg) grid = p.max_wg;
   if (grid > upper) grid = upper;
   if (grid >= 8) grid -= grid % 8;
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), kRing, s, p);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), kRing, s, q);
+  if (q.part_ks > 1)
+    hipLaunchKernelGGL(dense_part_reduce_kernel, dim3((unsigned)(groups * (p.N / 256))), dim3(256), 0, s, q);
   return hipGetLastError();
 }
 
 }  // namespace
+
+size_t dense_part_bytes(int64_t rows, int32_t groups, int32_t n, int32_t k) {
+  if (groups < 1 || groups > 256 || rows < (int64_t)kDenseMinAvgRows * groups) return 0;
+  if (n <= 0 || n % 256 != 0 || k % 128 != 0 || (k / kBK) % (4 * kPartKs) != 0 || k / kBK < 256) return 0;
+  const size_t need = part_need(groups, n / 256);
+  return need <= kPartBudget ? need : 0;
+}
 
 bool gemm_dense_eligible(const GemmProblem& p) {
   if (p.a_scale || p.x_rows != 0 || p.seg_end || (p.offsets && !p.rows_exact)) return false;

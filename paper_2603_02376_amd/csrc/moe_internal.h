@@ -81,7 +81,18 @@ struct GemmProblem {
   // Weight-streaming kernel only: at most this many workgroups (0: one per
   // compute unit), leaving compute units to kernels on other streams.
   int32_t max_wg;
+  // Compute-bound kernel, EPI_STORE with offsets: workspace for splitting the
+  // K range of the short remainder blocks (dense_part_bytes of it; nullptr:
+  // no split). See dense_part_bytes().
+  void* dense_part;
+  int64_t dense_part_bytes;
+  int32_t part_ks;  // set by the launcher: K parts of a remainder block (1: none)
 };
+
+// Workspace the compute-bound GEMM2 may use to split the K range of its
+// short remainder blocks, for an FFN of `groups` groups over `rows` rows with
+// output width n and reduction length k (0 when it never splits).
+size_t dense_part_bytes(int64_t rows, int32_t groups, int32_t n, int32_t k);
 
 // bf16 MFMA grouped GEMM (gfx950). out_f32 selects an fp32 output (EPI_STORE
 // only); otherwise outputs are bf16.

@@ -345,6 +345,10 @@ DENSE_CASES = [
     (600, 256, 1, 1, 128, None),       # one expert of 600 rows (88-row remainder: one wave row idle)
     (2049, 256, 4, 1, 128, 0),         # every token to expert 0: eight full blocks + one row; three empty experts
     (1540, 512, 3, 1, 640, None),      # ~513 rows: remainders of a few rows; GEMM2 K 640
+    # GEMM2 K >= 8192: the short remainder blocks split into four K parts, added by a second kernel
+    (1100, 256, 2, 1, 8192, None),     # ~550 rows: two full blocks + ~38 rows; one output column tile
+    (2200, 512, 4, 1, 8192, None),     # four remainders of ~20-80 rows, two output column tiles
+    (1400, 256, 2, 1, 8192, None),     # 715 + 685 rows: a 203-row remainder (full-cost block, no split), a 173-row one (split)
     # skewed (average below 512 rows, so the weight stream): one hot expert among small ones
     (1200, 512, 16, 2, 256, 0),        # one expert of 1,200 rows (7 passes), fifteen of ~80
     (700, 768, 32, 4, 384, 5),         # one of 700 rows (GEMM2 K 384), the others ~68
