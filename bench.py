@@ -552,9 +552,10 @@ def main():
         roof = dict(bound="mfma", achieved=round(r["ffn_tflops"], 1), peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
                     frac=round(r["ffn_tflops"] / MFMA_BF16_PEAK_TFLOPS, 4))
     roof["traffic"] = measured_traffic(args.workload, args.layout)
-    kern = ("weight-streaming GEMM1+SwiGLU and GEMM2 over packed weights" if args.layout == "packed"
-            else "tiled grouped GEMM1+SwiGLU and GEMM2 over row-major weights")
-    roof.update(kernel=f"moe_expert_ffn: {kern} (2 launches per call)",
+    kern = ("weight-streaming GEMM1+SwiGLU then GEMM2 over packed weights, one launch per call"
+            if args.layout == "packed" else "tiled grouped GEMM1+SwiGLU and GEMM2 over row-major weights, "
+            "2 launches per call")
+    roof.update(kernel=f"moe_expert_ffn: {kern}",
                 ms_per_call=round(r["ffn_ms"], 4), algorithmic_bytes=alg["ffn_bytes"],
                 algorithmic_flops=alg["ffn_flops"], touched_experts=alg["touched_experts"])
     out = {

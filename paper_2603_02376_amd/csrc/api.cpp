@@ -59,10 +59,15 @@ int gate_splits(const moe_config_t& c, int32_t T) {
   return (nkt + q - 1) / q;  // no empty split
 }
 
-// Tile-queue heads of the weight-streaming GEMMs: 8 per launch, GEMM1 and
-// GEMM2 of the routed FFN, then of the shared expert's own FFN (which may run
-// on another stream at the same time).
-constexpr int kQueueInts = 32;
+// Tile-queue heads of the weight-streaming GEMMs (8 per GEMM) and the
+// per-group counters of the one-launch FFN, all zeroed before use: the
+// routed FFN's GEMM1 and GEMM2 heads [0, 16) and counters [16, kRoutedInts),
+// then the heads of the shared expert's own FFN from kSharedQueue (that FFN
+// may run on another stream at the same time, so it has its own).
+constexpr int kRoutedInts = 16 + moe::kFfnDepsInts;
+constexpr int kSharedQueue = 288;
+constexpr int kQueueInts = kSharedQueue + 16;
+static_assert(kRoutedInts <= kSharedQueue, "queue regions overlap");
 
 // Byte offsets of every scratch region inside the caller's workspace.
 struct Layout {
@@ -267,8 +272,9 @@ struct FusedShared {
 // y = h Wdᵀ into `y`. packed: weights from moe_pack_weights (wu unused) and
 // the weight-streaming kernel; fused (packed only, same intermediate size):
 // the shared expert over all a_rows tokens rides along as an extra group.
-// queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path, zeroed
-// here unless queues_zeroed (moe_layer zeroes them in its dispatch).
+// queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path, then (with
+// one_launch) the one-launch FFN's counters, zeroed here unless queues_zeroed
+// (moe_layer zeroes them in its dispatch).
 // x_scales: x holds int8 codes of rows with these fp32 scales (packed only).
 // seg_end, max_wg (packed only): group g owns rows [offsets[g], seg_end[g]);
 // at most max_wg workgroups per GEMM (0: one per compute unit).
@@ -277,14 +283,18 @@ struct FusedShared {
 // kernel, whose choice does not depend on the groups' sizes).
 // dense_part: workspace in which the compute-bound GEMM2 may split the K
 // range of short remainder blocks (nullptr: never).
+// one_launch: run both weight-streaming GEMMs as one launch when the problem
+// allows it (bf16 tokens over whole groups, every compute unit), so the
+// end of GEMM1 overlaps the start of GEMM2.
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
                    void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
                    int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
                    int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false, bool rows_exact = true,
-                   void* dense_part = nullptr, size_t dense_part_bytes = 0) {
+                   void* dense_part = nullptr, size_t dense_part_bytes = 0, bool one_launch = false) {
+  one_launch = one_launch && packed && queues && !x_scales && !seg_end && max_wg == 0;
   if (packed && queues && !queues_zeroed) {
-    const hipError_t e = moe::launch_queue_reset(queues, 16, s);
+    const hipError_t e = moe::launch_queue_reset(queues, one_launch ? kRoutedInts : 16, s);
     if (e != hipSuccess) return e;
   }
   moe::GemmProblem up{};
@@ -312,8 +322,6 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   up.seg_end = seg_end;
   up.max_wg = max_wg;
   up.rows_exact = rows_exact && !seg_end ? 1 : 0;
-  hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
-  if (e != hipSuccess) return e;
   moe::GemmProblem down{};
   down.A = h;
   down.a_rows = rows;
@@ -337,6 +345,13 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   down.rows_exact = up.rows_exact;
   down.dense_part = dense_part;
   down.dense_part_bytes = (int64_t)dense_part_bytes;
+  if (one_launch) {
+    up.deps = down.deps = queues + 16;
+    const hipError_t e = moe::launch_ffn_stream(up, down, s);
+    if (e != hipErrorNotSupported) return e;  // otherwise nothing was launched
+  }
+  hipError_t e = packed ? moe::launch_gemm_stream(up, moe::EPI_SWIGLU, s) : run_gemm(c, up, moe::EPI_SWIGLU, false, s);
+  if (e != hipSuccess) return e;
   return packed ? moe::launch_gemm_stream(down, moe::EPI_STORE, s) : run_gemm(c, down, moe::EPI_STORE, false, s);
 }
 
@@ -583,7 +598,8 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
                                static_cast<char*>(ws) + L.h, y_perm, stream, packed, nullptr,
                                reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), nullptr, nullptr, 0,
-                               false, false, true, static_cast<char*>(ws) + L.dense_part, L.dense_part_bytes);
+                               false, false, true, static_cast<char*>(ws) + L.dense_part, L.dense_part_bytes,
+                               /*one_launch=*/true);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
 }
 
@@ -648,7 +664,7 @@ int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void
   const Layout L = make_layout(*cfg, T);
   const hipError_t e = run_ffn(*cfg, T, T, 1, cfg->I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down,
                                static_cast<char*>(ws) + L.shared_h, out, stream, packed, nullptr,
-                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues) + 16);
+                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues) + kSharedQueue);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "shared FFN");
 }
 
@@ -707,7 +723,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   int32_t* inv = d.inv_perm ? d.inv_perm : reinterpret_cast<int32_t*>(w + L.inv_perm);
   void* y = d.y_perm ? d.y_perm : w + L.y_perm;
   void* shared = c.n_shared ? (d.shared_out ? d.shared_out : w + L.shared_out) : nullptr;
-  int32_t* const queues = reinterpret_cast<int32_t*>(w + L.queues);  // routed FFN: [0, 16), shared FFN: [16, 32)
+  int32_t* const queues = reinterpret_cast<int32_t*>(w + L.queues);  // routed FFN from 0, shared FFN from kSharedQueue
 
   hipError_t e;
   // Packed weights with equal intermediate sizes: the shared expert runs
@@ -729,16 +745,17 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     if ((e = hipEventRecord(ev->fork, s_main)) != hipSuccess) return hip_fail(e, "event record");
     if ((e = hipStreamWaitEvent(s_aux, ev->fork, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h, shared,
-                     s_aux, packed, nullptr, queues + 16)) != hipSuccess)
+                     s_aux, packed, nullptr, queues + kSharedQueue)) != hipSuccess)
       return hip_fail(e, "shared FFN");
     if ((e = hipEventRecord(ev->join, s_aux)) != hipSuccess) return hip_fail(e, "event record");
   }
   if ((e = run_gate_route(c, T, x, w_router, bias, logits, reinterpret_cast<float*>(w + L.gate_partials), idx, tw,
                           s_main)) != hipSuccess)
     return hip_fail(e, "route");
-  // the dispatch also zeroes the routed FFN's 16 tile-queue heads (packed weights)
+  // the dispatch also zeroes the routed FFN's tile-queue heads and counters
+  // (packed weights; with quantized tokens also the shared GEMM1's heads)
   if ((e = run_dispatch(c, T, idx, w, L, counts, offsets, st, d.sorted_assign, inv, s_main, packed ? queues : nullptr,
-                        packed ? (fuse_down ? 24 : 16) : 0)) != hipSuccess)
+                        packed ? (fuse_down ? kSharedQueue + 8 : kRoutedInts) : 0)) != hipSuccess)
     return hip_fail(e, "dispatch");
   int8_t* const qcodes = reinterpret_cast<int8_t*>(w + L.qcodes);
   float* const qscales = reinterpret_cast<float*>(w + L.qscales);
@@ -751,7 +768,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     fs.h = w + L.shared_h;
     fs.out = shared;
   }
-  if (fuse_down) {  // the shared expert's GEMM1 on its own (queue heads 16..23, zeroed by the dispatch)
+  if (fuse_down) {  // the shared expert's GEMM1 on its own (queue heads from kSharedQueue, zeroed by the dispatch)
     moe::GemmProblem g{};
     g.A = x;
     g.a_rows = T;
@@ -762,20 +779,20 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     g.K = c.d;
     g.C = fs.h;
     g.ldc = c.I_shared;
-    g.tile_queue = queues + 16;
+    g.tile_queue = queues + kSharedQueue;
     if ((e = moe::launch_gemm_stream(g, moe::EPI_SWIGLU, s_main)) != hipSuccess) return hip_fail(e, "shared GEMM1");
   }
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
                    w_down, w + L.h, y, s_main, packed, (fuse || fuse_down) ? &fs : nullptr, queues,
                    q8 ? qscales : nullptr, nullptr, 0, f8, /*queues_zeroed=*/true, /*rows_exact=*/true,
-                   w + L.dense_part, L.dense_part_bytes)) !=
+                   w + L.dense_part, L.dense_part_bytes, /*one_launch=*/true)) !=
       hipSuccess)
     return hip_fail(e, "expert FFN");
   if (own) {
     if (two) {
       if ((e = hipStreamWaitEvent(s_main, ev->join, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     } else if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h,
-                            shared, s_main, packed, nullptr, queues + 16)) != hipSuccess) {
+                            shared, s_main, packed, nullptr, queues + kSharedQueue)) != hipSuccess) {
       return hip_fail(e, "shared FFN");
     }
   }

@@ -42,6 +42,14 @@
 //     and share the weight stream through L2.
 //   * The K loop is compiled per count of active 32-row fragments, so the
 //     MFMA stream has no branches.
+//   * The expert FFN is one launch (ffn_stream_kernel): every workgroup
+//     takes GEMM1 tiles until none is left anywhere, then GEMM2 tiles. A
+//     GEMM2 tile first waits until every GEMM1 tile of its group has counted
+//     its (complete) stores of h; groups finish in tile-list order, so the
+//     wait is rare and short, and the compute units that run out of GEMM1
+//     work start on GEMM2 instead of idling until the slowest GEMM1 tile is
+//     done. Every tile is claimed from the queues, so a tile that a wait
+//     depends on is always held by a running workgroup.
 //   * The MFMAs take the weights as their first operand and the token rows
 //     as their second, so every lane ends with runs of 4 consecutive output
 //     columns of one token row. The epilogue assembles the output tile in
@@ -180,19 +188,46 @@ __device__ __forceinline__ int scan4(int v, int* scratch, int* total) {
   return base + inc - v;
 }
 
+// Role of one GEMM in a launch: alone, or a phase of the fused FFN launch
+// (ffn_stream_kernel): GEMM1 there counts its finished tiles per group
+// (PRODUCER), GEMM2 waits for them before reading a group's rows of h
+// (CONSUMER). In both phases every tile is claimed from the queues (none is
+// implicitly a workgroup's first), so a tile that a wait depends on is always
+// held by a running workgroup.
+enum { ROLE_ALONE = 0, ROLE_PRODUCER = 1, ROLE_CONSUMER = 2 };
+// Polls of a GEMM2 tile's wait (each followed by a short sleep) before it sets
+// the wait flag and goes on: about a second, thousands of times any real wait.
+constexpr int kWaitPolls = 1 << 22;
+
+// A counter of the fused launch as this moment's value at the coherence
+// point: an atomic max with 0 (no change to a non-negative counter). A plain
+// load, even an atomic one, may be served from a line that this XCD's L2
+// still holds from an earlier read, and a line read that often stays there.
+__device__ __forceinline__ int read_counter(int32_t* c) {
+  return __hip_atomic_fetch_max(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Per-workgroup bookkeeping in static LDS, one copy per launch (the two
+// phases of the fused launch use it in turn).
+struct StreamLds {
+  int tstart[257];            // first tile (pass) of each group
+  int scan_scratch[kWaves];
+  int next;                   // the workgroup's next tile
+  int ready;                  // CONSUMER: every workgroup is done with GEMM1
+};
+
 // EPI_SWIGLU: GEMM1 (j = gate/up, 32 output columns per wave);
 // EPI_STORE:  GEMM2 (j = two 32-column halves, 64 output columns per wave).
-template <int EPI, bool Q8, bool F8, bool DEEP>
-__global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
+template <int EPI, bool Q8, bool F8, bool DEEP, int ROLE>
+__device__ __forceinline__ void stream_gemm(const GemmProblem& p, char* smem, StreamLds& sl) {
   constexpr int kMaxRows = StreamCfg<DEEP>::rows, kDepth = StreamCfg<DEEP>::depth;
   constexpr int kSlots = StreamCfg<DEEP>::slots, kUnroll = StreamCfg<DEEP>::unroll;
   static_assert(kUnroll % kDepth == 0 && kUnroll % kSlots == 0 && kUnroll % kStage == 0, "unroll");
   constexpr int WCOLS = (EPI == EPI_SWIGLU) ? 32 : 64;  // output columns per wave
   constexpr int TCOLS = WCOLS * kWaves;                  // per tile
-  // Dynamic LDS: the A ring (kSlots slots of kMaxRows x 128 bytes).
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  __shared__ int tstart[257];
-  __shared__ int scan_scratch[kWaves];
+  // smem (dynamic LDS): the A ring (kSlots slots of kMaxRows x 128 bytes).
+  int(&tstart)[257] = sl.tstart;
+  int* const scan_scratch = sl.scan_scratch;
   __shared__ float s_scale[kMaxRows];  // Q8: the tile's row scales
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -219,11 +254,15 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   // extra group's passes of column tile j side by side (adjacent tiles run on
   // one XCD at the same time and share that weight stream through its L2),
   // so the extra group's compute-heavy full passes run next to memory-heavy
-  // routed ones rather than all at the end.
+  // routed ones rather than all at the end. GEMM1 of the fused launch puts
+  // the passes of two column tiles in each of the first Nt/2 segments, so
+  // the extra group's GEMM1 is done by mid-launch and its GEMM2 tiles never
+  // wait.
+  constexpr int XD = (ROLE == ROLE_PRODUCER) ? 2 : 1;  // column tiles' extra passes per segment
   const int routed_tiles = tstart[groups] * Nt;
   const int units_x = (p.x_rows + kMaxRows - 1) / kMaxRows;
   const int total_tiles = routed_tiles + Nt * units_x;
-  auto seg_start = [&](int j) { return (int)((int64_t)j * routed_tiles / Nt) + j * units_x; };
+  auto seg_start = [&](int j) { return (int)((int64_t)j * routed_tiles / Nt) + units_x * min(j * XD, Nt); };
   const int nk = p.K / 64;
   // Rows [row0, row0 + rows) of pass `pass` of a group of c rows taking
   // `passes` passes: the group's 32-row fragments are spread evenly over its
@@ -243,11 +282,39 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   // and then claims entries W, W + 1, ... from its XCD's queue head; when its
   // queue is empty it takes tiles from the other XCDs' queues. Without queue
   // heads it takes every G-th tile.
-  const bool dyn = p.tile_queue != nullptr && G % 8 == 0;
+  const bool dyn = p.tile_queue != nullptr && G % 8 == 0;  // always, in the fused launch
   const int W = G / 8, xcd = b % 8;
   auto qtile = [&](int x, int q) { return (q / W) * G + x * W + q % W; };
   const int vb = (G % 8 == 0) ? xcd * W + (b / 8) : b;
-  __shared__ int s_next;
+  constexpr bool CLAIM_ALL = ROLE != ROLE_ALONE;
+  const int q0 = CLAIM_ALL ? 0 : W;  // queue entries below q0 are the workgroups' implicit first tiles
+  int& s_next = sl.next;
+  // this XCD's queue is empty: take a tile from another XCD's queue
+  auto steal = [&](int& tile) __attribute__((always_inline)) {
+    if (dyn && tile >= total_tiles) {
+      __syncthreads();  // every thread has read s_next
+      if (tid == 0) {
+        int t = total_tiles;
+        for (int k = 1; k < 8 && t >= total_tiles; ++k) {
+          const int x = (xcd + k) % 8;
+          t = qtile(x, q0 + atomicAdd(&p.tile_queue[x], 1));
+        }
+        s_next = t;
+      }
+      __syncthreads();
+      tile = s_next;
+    }
+  };
+  int tile = vb;
+  if constexpr (CLAIM_ALL) {
+    if (tid == 0) s_next = qtile(xcd, atomicAdd(&p.tile_queue[xcd], 1));
+    __syncthreads();
+    tile = s_next;
+    steal(tile);
+  }
+  int pend = -1;  // PRODUCER: group of the previous tile, counted once its stores are complete
+  int& s_ready = sl.ready;
+  bool ready = false;  // CONSUMER: every workgroup is done with GEMM1 (no tile needs to wait)
   const int K = p.K;
   // A rows move in 1 KB blocks of 8 rows (block b of a wave: rows 32b + 8 wave
   // + 0..7): lane l carries row l/8 of the block and the logical 16-byte chunk
@@ -258,7 +325,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
   // and codes 16 (l%4) .. 16 (l%4) + 15 of the step's 64.
   const int lr8 = lane >> 2, lc8 = lane & 3;
 
-  for (int tile = vb; tile < total_tiles;) {
+  while (tile < total_tiles) {
     // claim the next entry of this XCD's queue now; it is used after this tile
     int claim = 0;
     if (dyn && tid == 0) claim = atomicAdd(&p.tile_queue[xcd], 1);
@@ -275,19 +342,21 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     const int r_beg = (int)((int64_t)seg * routed_tiles / Nt);
     const int r_len = (int)((int64_t)(seg + 1) * routed_tiles / Nt) - r_beg;
     const int off = units_x > 0 ? tile - seg_start(seg) : tile;
-    const bool extra = units_x > 0 && off >= r_len;  // pass off - r_len of the extra group, column tile seg
+    const bool extra = units_x > 0 && off >= r_len;  // extra-group tile off - r_len of segment seg
     const void* a_base;
     const int32_t* gather;
     int a_rows, row0, rows, nt;
     const char* b_base;
     __bf16* c_base;
     bool multi;  // the tile's group takes more than one pass
+    int gid;     // the tile's group (the extra group: groups)
     if (extra) {
       a_base = p.xA;
       a_rows = p.x_rows;
       gather = nullptr;
-      nt = seg;
-      pass_rows(p.x_rows, units_x, off - r_len, row0, rows);
+      nt = seg * XD + (off - r_len) / units_x;
+      gid = groups;
+      pass_rows(p.x_rows, units_x, (off - r_len) % units_x, row0, rows);
       multi = units_x > 1;
       b_base = static_cast<const char*>(p.xB) + (size_t)nt * nk * kWaves * kStepBytes;
       c_base = static_cast<__bf16*>(p.xC);
@@ -301,6 +370,7 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
         if (tstart[mid] <= q) lo = mid; else hi = mid - 1;
       }
       const int e = lo;
+      gid = e;
       const int local = rt - tstart[e] * Nt;
       const int passes = tstart[e + 1] - tstart[e];
       const int pass = local % passes;
@@ -315,6 +385,40 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       row0 += gbeg;
       b_base = static_cast<const char*>(p.B0) + ((size_t)e * Nt + nt) * nk * kWaves * kStepBytes;
       c_base = static_cast<__bf16*>(p.C);
+    }
+    if constexpr (ROLE == ROLE_CONSUMER) {
+      // Wait until every GEMM1 tile of this group (its passes of up to 192
+      // rows x its N/128 column tiles, the same rows and count in GEMM1's
+      // tile list) has stored its rows of h. Those stores are written
+      // through to memory and complete before their count is added. No L2
+      // holds an older copy of the rows: the caches start the launch without
+      // them and this launch reads them only after the wait, so the loads
+      // below see the new values. Once every workgroup is done with GEMM1
+      // (the count at groups + 2 reaches the grid), no tile checks again.
+      if (!ready) {
+        if (tid == 0) {
+          int r = read_counter(p.deps + groups + 2) >= G;
+          if (!r) {
+            int c = p.x_rows;
+            if (!extra) {
+              const int lo = min(max(p.offsets[gid], 0), p.M);
+              c = min(max(p.offsets[gid + 1], lo), p.M) - lo;
+            }
+            constexpr int kRows1 = StreamCfg<false>::rows, kCols1 = 32 * kWaves;  // GEMM1 pass rows, tile columns
+            const int need = (c + kRows1 - 1) / kRows1 * (K / kCols1);
+            for (int it = 0; read_counter(p.deps + gid) < need; ++it) {
+              if (it == kWaitPolls) {
+                __hip_atomic_fetch_or(p.deps + groups + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+              }
+              __builtin_amdgcn_s_sleep(8);
+            }
+          }
+          s_ready = r;
+        }
+        __syncthreads();
+        ready = s_ready;
+      }
     }
     const __amdgpu_buffer_rsrc_t a_rs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<void*>(a_base), (short)0, (int)(uint32_t)((size_t)a_rows * K * (Q8 ? 1 : 2)), 0x00020000);
@@ -526,8 +630,18 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
     {
       constexpr int OCH = TCOLS * 2 / 16;      // 16-byte chunks per output row
       constexpr int OROWS = kThreads / OCH;    // rows per store pass
-      if (tid == 0) s_next = dyn ? qtile(xcd, W + claim) : tile + G;
+      if (tid == 0) s_next = dyn ? qtile(xcd, q0 + claim) : tile + G;
+      // PRODUCER: the previous tile's stores (issued a whole tile ago) are
+      // complete; no load is in flight at this point (the K loop's last
+      // steps skip every load past the last step)
+      if constexpr (ROLE == ROLE_PRODUCER) {
+        if (pend >= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      }
       lds_barrier();                           // every wave is done reading the A ring
+      if constexpr (ROLE == ROLE_PRODUCER) {
+        if (pend >= 0 && tid == 0) __hip_atomic_fetch_add(p.deps + pend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        pend = gid;
+      }
       const int h = lane >> 5;
 #pragma unroll
       for (int i = 0; i < kMaxRows / 32; ++i) {
@@ -580,25 +694,42 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p)
       }
     }
     tile = s_next;  // written before the epilogue's barriers
-    if (dyn && tile >= total_tiles) {
-      // this XCD's queue is empty: take a tile from another XCD's queue
-      __syncthreads();  // every thread has read s_next
-      if (tid == 0) {
-        int t = total_tiles;
-        for (int k = 1; k < 8 && t >= total_tiles; ++k) {
-          const int x = (xcd + k) % 8;
-          t = qtile(x, W + atomicAdd(&p.tile_queue[x], 1));
-        }
-        s_next = t;
-      }
-      __syncthreads();
-      tile = s_next;
+    steal(tile);
+  }
+  if constexpr (ROLE == ROLE_PRODUCER) {
+    // the last tile's count, once every thread's stores are complete, then
+    // (after that count is performed) this workgroup's end of GEMM1
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+      if (pend >= 0) __hip_atomic_fetch_add(p.deps + pend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __hip_atomic_fetch_add(p.deps + groups + 2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    __syncthreads();  // the LDS and s_next are free for the next phase
   }
 }
 
+template <int EPI, bool Q8, bool F8, bool DEEP>
+__global__ void __launch_bounds__(kThreads, 1) gemm_stream_kernel(GemmProblem p) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ StreamLds sl;
+  stream_gemm<EPI, Q8, F8, DEEP, ROLE_ALONE>(p, smem, sl);
+}
+
+// The expert FFN in one launch: GEMM1+SwiGLU over bf16 tokens, then GEMM2
+// (DEEP2: its deep pipeline shape) on the same workgroups, so the end of
+// GEMM1 overlaps the start of GEMM2 instead of idling compute units.
+template <bool DEEP2>
+__global__ void __launch_bounds__(kThreads, 1) ffn_stream_kernel(GemmProblem up, GemmProblem down) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ StreamLds sl;
+  stream_gemm<EPI_SWIGLU, false, false, false, ROLE_PRODUCER>(up, smem, sl);
+  stream_gemm<EPI_STORE, false, false, DEEP2, ROLE_CONSUMER>(down, smem, sl);
+}
+
 __global__ void queue_reset_kernel(int32_t* q, int n) {
-  if ((int)threadIdx.x < n) q[threadIdx.x] = 0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) q[i] = 0;
 }
 
 // One 16-byte chunk per thread: packed position -> source row and k.
@@ -682,9 +813,62 @@ hipError_t launch_gemm_stream(const GemmProblem& p, int epi, hipStream_t s) {
 }
 
 hipError_t launch_queue_reset(int32_t* q, int n, hipStream_t s) {
-  if (!q || n <= 0 || n > 64) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(queue_reset_kernel, dim3(1), dim3(64), 0, s, q, n);
+  if (!q || n <= 0 || n > 4096) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(queue_reset_kernel, dim3(1), dim3(256), 0, s, q, n);
   return hipGetLastError();
+}
+
+namespace {
+
+template <bool DEEP2>
+hipError_t launch_ffn(const GemmProblem& up, const GemmProblem& down, long long grid, hipStream_t s) {
+  auto kern = ffn_stream_kernel<DEEP2>;
+  // the larger of the two phases' LDS (each phase's ring, reused as its output tile)
+  constexpr size_t lds1 = std::max<size_t>((size_t)StreamCfg<false>::slots * StreamCfg<false>::rows * 128,
+                                           (size_t)StreamCfg<false>::rows * 128 * 2);
+  constexpr size_t lds2 = std::max<size_t>((size_t)StreamCfg<DEEP2>::slots * StreamCfg<DEEP2>::rows * 128,
+                                           (size_t)StreamCfg<DEEP2>::rows * 256 * 2);
+  constexpr size_t lds = std::max(lds1, lds2);
+  static std::once_flag once;
+  static hipError_t init_err = hipSuccess;
+  std::call_once(once, [&] {
+    init_err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  });
+  if (init_err != hipSuccess) return init_err;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, s, up, down);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ffn_stream(const GemmProblem& up, const GemmProblem& down, hipStream_t s) {
+  // bf16 tokens, whole groups of a dispatch, the compute units to itself,
+  // and a weight-streaming problem in both GEMMs (nothing is launched when
+  // it does not fit: the caller then makes the two launches)
+  if (!up.deps || up.deps != down.deps || !up.tile_queue || !down.tile_queue || !up.offsets ||
+      up.offsets != down.offsets || up.groups != down.groups || up.groups < 1 || up.groups > kFfnDepsInts - 3)
+    return hipErrorNotSupported;
+  if (up.a_scale || up.seg_end || down.seg_end || up.max_wg || down.max_wg || up.x_rows != down.x_rows ||
+      up.N != down.K || up.M != down.M)
+    return hipErrorNotSupported;
+  if (gemm_dense_eligible(up) || gemm_dense_eligible(down)) return hipErrorNotSupported;
+  if (up.N % 128 != 0 || down.N % 256 != 0 || up.K % 64 != 0 || down.K % 64 != 0) return hipErrorInvalidValue;
+  // A is addressed through buffer resources: 32-bit byte offsets
+  if ((size_t)up.a_rows * (size_t)up.K * 2 > 0xFFFFFFFFull || (size_t)up.x_rows * (size_t)up.K * 2 > 0xFFFFFFFFull ||
+      (size_t)down.a_rows * (size_t)down.K * 2 > 0xFFFFFFFFull ||
+      (size_t)down.x_rows * (size_t)down.K * 2 > 0xFFFFFFFFull)
+    return hipErrorInvalidValue;
+  if (up.x_rows < 0 || (up.x_rows > 0 && (!up.xA || !up.xB || !up.xC || !down.xA || !down.xB || !down.xC)))
+    return hipErrorInvalidValue;
+  const bool small = (long long)down.M <= (long long)kDeepMaxAvgRows * down.groups;
+  const int rows1 = StreamCfg<false>::rows, rows2 = small ? StreamCfg<true>::rows : StreamCfg<false>::rows;
+  const long long upper1 = ((up.M + rows1 - 1) / rows1 + up.groups + (up.x_rows + rows1 - 1) / rows1) * (up.N / 128);
+  const long long upper2 =
+      ((down.M + rows2 - 1) / rows2 + down.groups + (down.x_rows + rows2 - 1) / rows2) * (down.N / 256);
+  long long grid = std::min<long long>(device_cu_count(), std::max(upper1, upper2));
+  grid -= grid % 8;
+  if (grid < 8) return hipErrorNotSupported;  // the tile queues need a multiple of 8 workgroups
+  return small ? launch_ffn<true>(up, down, grid, s) : launch_ffn<false>(up, down, grid, s);
 }
 
 hipError_t launch_pack(const void* w0, const void* w1, void* dst, int E, int N, int K, bool gate_up, hipStream_t s) {

@@ -87,7 +87,17 @@ struct GemmProblem {
   void* dense_part;
   int64_t dense_part_bytes;
   int32_t part_ks;  // set by the launcher: K parts of a remainder block (1: none)
+  // Weight-streaming FFN launch (launch_ffn_stream) only: completion
+  // counters, zero at launch: [g] counts the finished GEMM1 tiles of group g
+  // (the extra group at [groups]); [groups + 1] is set when a GEMM2 tile gave
+  // up waiting for its rows (never, unless tiles are lost); [groups + 2]
+  // counts the workgroups done with GEMM1.
+  int32_t* deps;
 };
+
+// Ints of the completion counters of a fused FFN launch: up to 256 groups,
+// the extra group, the wait flag, the finished-workgroup count.
+constexpr int kFfnDepsInts = 260;
 
 // Workspace the compute-bound GEMM2 may use to split the K range of its
 // short remainder blocks, for an FFN of `groups` groups over `rows` rows with
@@ -111,6 +121,15 @@ hipError_t launch_gemm_dense(const GemmProblem& p, int epilogue, hipStream_t s);
 // Zeroes n queue heads of launch_gemm_stream (a one-workgroup kernel, so
 // it can be captured in a graph).
 hipError_t launch_queue_reset(int32_t* q, int n, hipStream_t s);
+
+// The whole weight-streaming expert FFN in one launch: every workgroup runs
+// GEMM1 tiles (up: EPI_SWIGLU, bf16 tokens) until none is left, then GEMM2
+// tiles (down: EPI_STORE), each of which first waits until every GEMM1 tile
+// of its group has stored its rows of h. up.deps (== down.deps, zero at
+// launch) holds the counters; up.tile_queue and down.tile_queue 8 zeroed
+// heads each. Returns hipErrorNotSupported when the problem does not fit
+// this launch (the caller then runs the two GEMMs as separate launches).
+hipError_t launch_ffn_stream(const GemmProblem& up, const GemmProblem& down, hipStream_t s);
 // Packs [E][N][K] row-major weights (gate_up: w0 = gate, w1 = up) into the
 // streaming kernel's layout.
 hipError_t launch_pack(const void* w0, const void* w1, void* dst, int E, int N, int K, bool gate_up, hipStream_t s);

@@ -375,3 +375,37 @@ def test_expert_ffn_packed(case):
     err = max_rel_err(got, want)
     log("  max_rel_err", err)
     assert err <= BF16_TOL
+
+
+def test_expert_ffn_packed_queued_calls():
+    """Weight-streaming FFN calls queued on one workspace without a sync
+    between them: the one-launch FFN's per-group counters are zeroed again by
+    each call (a count left over would let GEMM2 read h rows before GEMM1
+    stored them), so every call matches the oracle and a repeated call gives
+    the same bits."""
+    T, d, E, k, I = 1536, 256, 16, 4, 640
+    log("expert_ffn packed, queued calls", (T, d, E, k, I))
+    p = dict(T=T, d=d, E=E, k=k, I=I, dtype="bf16", n_shared=0, bias="none")
+    t = inputs.make_inputs(p, 3, "cuda")
+    cfg = moe.MoeConfig(d=d, E=E, k=k, I=I, dtype="bf16", weight_layout="packed")
+    gu, dn = moe.pack_weights(cfg, t["w_gate"], t["w_up"], t["w_down"])
+    ws = moe.alloc_workspace(cfg, T)
+    routings = [_random_topk(T, E, k, np.random.default_rng(11)),
+                _random_topk(T, E, k, np.random.default_rng(12), hot=5),  # a hot expert: multi-pass groups
+                _random_topk(T, E, k, np.random.default_rng(11))]
+    plans = [O.dispatch(idx, E) for idx in routings]
+    ys = [torch.full((T * k, d), float("nan"), dtype=torch.bfloat16, device="cuda") for _ in plans]
+    dev = [(_dev(st), _dev(off)) for _, off, st, _, _ in plans]
+    torch.cuda.synchronize()
+    for (st_d, off_d), y in zip(dev, ys):
+        moe.moe_expert_ffn(cfg, T, t["x"], st_d, off_d, gu, None, dn, y, ws)
+    torch.cuda.synchronize()
+    xv = inputs.oracle_view(t["x"])
+    wv = (inputs.ExpertView(t["w_gate"]), inputs.ExpertView(t["w_up"]), inputs.ExpertView(t["w_down"]))
+    for n, ((_, offsets, st, _, _), y) in enumerate(zip(plans[:2], ys[:2])):
+        got = host(y.float())
+        assert np.isfinite(got).all(), f"call {n}: rows left unwritten"
+        err = max_rel_err(got, O.expert_ffn(xv, st, offsets, *wv))
+        log(f"  call {n} max_rel_err", err)
+        assert err <= BF16_TOL
+    assert torch.equal(ys[0], ys[2]), "the repeated call changed bits"
