@@ -111,13 +111,16 @@ def test_layer_on_side_streams():
     assert torch.equal(ref["out"], r["out"])
 
 
-@pytest.mark.parametrize("two_streams", [False, True])
-def test_layer_fused_shared_equals_composed_calls(two_streams):
+@pytest.mark.parametrize("two_streams,I", [(False, 256), (True, 256), (False, 384)])
+def test_layer_fused_shared_equals_composed_calls(two_streams, I):
     # moe_layer with packed weights runs the shared expert inside the routed
     # GEMMs; composing the layer from the public calls (route, dispatch, routed
     # FFN, shared FFN on the same or a second stream, combine) must give the
-    # same bits: every output element is summed in the same order.
-    p = dict(SMALL["dsv3_like_bf16"], d=512, I=256, I_shared=256, weight_layout="packed")
+    # same bits: every output element is summed in the same order. I = 384:
+    # three GEMM1 column tiles, so the one-launch FFN's GEMM1 puts the shared
+    # expert's passes of two column tiles in its first segment and of the
+    # third in the second.
+    p = dict(SMALL["dsv3_like_bf16"], d=512, I=I, I_shared=I, weight_layout="packed")
     t = G.device_inputs(p, seed=6)
     ref = G.run_layer(p, t)
     cfg = G.moe_cfg(p)
