@@ -476,6 +476,42 @@ def cpu_baseline(p, t, n_experts: int = CPU_EXPERTS):
                         f"time scaled by {n_touched}/{len(chosen)} to the whole layer"))
 
 
+def library_gemm_reference(steps: int, warmup: int) -> dict:
+    """Reference only, not part of the measured path: the vendor library
+    (torch.matmul, hipBLASLt) on the Mixtral-shaped GEMM1 (d = 4096 into
+    2 x 14336 gate and up columns, bf16), for one expert's 1,024 rows, for
+    all 8,192 routed rows through one weight matrix, and for the 8 experts'
+    1,024-row GEMMs batched (the grouped problem the expert FFN solves)."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    d, n, rows, E = 4096, 2 * 14336, 1024, 8
+    a = torch.randn((E, rows, d), generator=g, device="cuda").to(torch.bfloat16)
+    b = (torch.randn((E, d, n), generator=g, device="cuda") * 0.02).to(torch.bfloat16)  # contiguous, not a view
+    out = {}
+    cases = {"one_expert": (lambda: torch.matmul(a[0], b[0]), 2.0 * rows * d * n),
+             "all_rows_one_weight": (lambda: torch.matmul(a.view(E * rows, d), b[0]), 2.0 * E * rows * d * n),
+             "grouped_8_experts": (lambda: torch.matmul(a, b), 2.0 * E * rows * d * n)}
+    for key, (fn, flops) in cases.items():
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        out[key + "_tflops"] = round(flops / (ms * 1e-3) / 1e12, 1)
+    del a, b
+    torch.cuda.empty_cache()
+    out["note"] = ("torch.matmul (hipBLASLt) on the Mixtral GEMM1 shape (d 4096 -> 2 x 14336, bf16), same run, for "
+                   "reference: one expert's 1,024 rows; all 8,192 routed rows through one weight; the 8 experts' "
+                   "GEMMs batched")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -540,6 +576,9 @@ def main():
             for key in ("int8_tokens", "fp8_tokens"):
                 if r[key]:
                     extra[name][key] = r[key]
+            if name == "mixtral":
+                log("[bench] mixtral: library GEMM reference")
+                extra[name]["library_gemm1"] = library_gemm_reference(args.steps, args.warmup)
 
     r = main_res
     p = r["p"]
