@@ -11,9 +11,12 @@
 //     columns with their gate and up rows; GEMM2: 256 output columns), one
 //     workgroup of 8 waves per compute unit (two per SIMD, so one wave's LDS
 //     and barrier waits are covered by the other's MFMAs), each wave 128
-//     token rows x 64 weight columns (8 accumulator tiles of 32x32 in
-//     AGPRs). A K step of 32 feeds every wave 16 MFMAs
-//     (v_mfma_f32_32x32x16_bf16) from 12 fragment reads.
+//     token rows x 64 weight columns (32 accumulator tiles of 16x16). A K
+//     step of 32 feeds every wave 32 MFMAs (v_mfma_f32_16x16x32_bf16) from
+//     12 fragment reads: the same operand bytes and matrix-core cycles as
+//     the 32x32x16 form, but the chip holds a higher clock under it (it
+//     runs at its power limit here, and this instruction costs less energy
+//     per FLOP).
 //   * Both operands go through a 4-slot LDS ring of 32 KB (16 KB of token
 //     rows, 16 KB of weights per step) filled by direct global->LDS loads
 //     (buffer_load_dwordx4 ... lds): no register staging, loads issued three
@@ -267,13 +270,14 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
           ((kx0 + x) >> 1) * 32768 + ((kx0 + x) & 1) * 4096, 0, 0);
     };
 
-    f32x16 acc[4][2];
+    // acc[f][wc]: 16 token rows (fragment f) x 16 weight columns (fragment wc)
+    f32x4 acc[8][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int f = 0; f < 8; ++f)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int wc = 0; wc < 4; ++wc)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+        for (int r = 0; r < 4; ++r) acc[f][wc][r] = 0.f;
     // active 32-row fragments of this wave: fragment i covers rows (wm + 2 i) * 32 ..
     const int nfrag = (rows + 31) / 32;
     const int nact = __builtin_amdgcn_readfirstlane((nfrag - wm + 1) / 2);
@@ -293,23 +297,34 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
       load_step(0, 0);
       load_step(1, 1);
       load_step(2, 2);
-      i32x4 af[2][NACT > 0 ? NACT : 1], bf[2][2];
-      // fragments of K slice kk (0 or 1) of slot s into register set sel
-      auto read_frags = [&](int s, int kk, int sel) __attribute__((always_inline)) {
-        const char* const as = smem + s * kSlotBytes;
-        const char* const bs = as + kABytes;
-#pragma unroll
-        for (int i = 0; i < NACT; ++i)
-          af[sel][i] = *reinterpret_cast<const i32x4*>(as + a_off((wm + 2 * i) * 32 + (lane & 31), 2 * kk + (lane >> 5)));
-#pragma unroll
-        for (int j = 0; j < 2; ++j)  // weight slot wn, gate/up (or column half) j
-          bf[sel][j] = *reinterpret_cast<const i32x4*>(bs + (((wn * 2 + kk) * 2 + j) << 10) + lane * 16);
+      // Fragments of v_mfma_f32_16x16x32_bf16 (weights as the first operand:
+      // lane l supplies weight column l % 16, token row l % 16, and the 8 K
+      // values 8 (l / 16) .. + 7 of the 32-wide step). Token fragment f: rows
+      // (wm + 2 (f / 2)) * 32 + (f % 2) * 16 + 0..15; weight fragment wc:
+      // columns (wc % 2) * 16 + 0..15 of j = wc / 2 (gate / up, or column
+      // half) of packed wave slot wn.
+      constexpr int NF = 2 * NACT;
+      i32x4 wf[4], tf[2];  // weight fragments; a ring of token fragments
+      auto read_t = [&](int s, int f) __attribute__((always_inline)) {
+        return *reinterpret_cast<const i32x4*>(smem + s * kSlotBytes +
+                                               a_off((wm + 2 * (f >> 1)) * 32 + (f & 1) * 16 + (lane & 15), lane >> 4));
       };
-      // Step x (slot U = x % 4): MFMAs of its two K slices, the reads of the
-      // second slice and of the next step's first, and (LOAD) the loads of
-      // step x + 3 into slot (U + 3) % 4, spread between the MFMAs. WAIT: 2 =
-      // wait for step x + 2's loads (younger: step x + 3's) then barrier;
-      // 1 = wait for all loads then barrier; 0 = neither.
+      // the packed 1 KB block (wn, K slice k, j) holds column c, K 8 h .. 8 h + 7 of the slice in lane 32 h + c
+      auto read_w = [&](int s, int wc) __attribute__((always_inline)) {
+        const int g = lane >> 4;  // K group: slice g / 2, half g % 2
+        return *reinterpret_cast<const i32x4*>(smem + s * kSlotBytes + kABytes +
+                                               (((wn * 2 + (g >> 1)) * 2 + (wc >> 1)) << 10) +
+                                               ((g & 1) * 32 + (wc & 1) * 16 + (lane & 15)) * 16);
+      };
+      // Step x (slot U = x % 4): token fragment by token fragment, its four
+      // MFMAs (one per weight fragment), the read of the next token fragment
+      // (past the last one: the next step's first, PRE) and (LOAD)
+      // a share of the loads of step x + 3 into slot (U + 3) % 4; with the
+      // last token fragment each weight fragment, once its last MFMA is
+      // issued, is replaced by the next step's (PRE). Token fragment f sits
+      // in ring entry f % 2 (NF is even).
+      // WAIT: 2 = wait for step x + 2's loads (younger: step x + 3's) then
+      // barrier; 1 = wait for all loads then barrier; 0 = neither.
       auto step = [&](int x, auto u_c, auto load_c, auto pre_c, auto wait_c) __attribute__((always_inline)) {
         constexpr int U = decltype(u_c)::value;
         constexpr bool LOAD = decltype(load_c)::value, PRE = decltype(pre_c)::value;
@@ -317,27 +332,25 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
         constexpr int LS = (U + 3) % kSlots;
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (NACT > 0) {
-          read_frags(U, 1, 1);
 #pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
+          for (int f = 0; f < NF; ++f) {
 #pragma unroll
-            for (int i = 0; i < NACT; ++i) {
-#pragma unroll
-              for (int j = 0; j < 2; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, bf[kk][j]),
-                                                                    __builtin_bit_cast(bf16x8, af[kk][i]), acc[i][j], 0,
-                                                                    0, 0);
-              if constexpr (LOAD) {  // the step's loads spread over the row fragments and K slices
-                constexpr int per = (LOADS + 2 * NACT - 1) / (2 * NACT);
-#pragma unroll
-                for (int n = (kk * NACT + i) * per; n < (kk * NACT + i + 1) * per && n < LOADS; ++n) {
-                  if (n < AL) load_a(x + 3, LS, n);
-                  else load_b(x + 3, LS, n - AL);
-                }
-              }
-              __builtin_amdgcn_sched_barrier(0);
+            for (int wc = 0; wc < 4; ++wc) {
+              acc[f][wc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wf[wc]),
+                                                                   __builtin_bit_cast(bf16x8, tf[f & 1]),
+                                                                   acc[f][wc], 0, 0, 0);
+              if (f == NF - 1 && PRE) wf[wc] = read_w((U + 1) % kSlots, wc);
             }
-            if (kk == 0 && PRE) read_frags((U + 1) % kSlots, 0, 0);
+            if (f + 1 < NF) tf[(f + 1) & 1] = read_t(U, f + 1);
+            else if (PRE) tf[0] = read_t((U + 1) % kSlots, 0);
+            if constexpr (LOAD) {  // the step's loads, spread over the fragments
+#pragma unroll
+              for (int n = f * LOADS / NF; n < (f + 1) * LOADS / NF; ++n) {
+                if (n < AL) load_a(x + 3, LS, n);
+                else load_b(x + 3, LS, n - AL);
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
           }
         } else if constexpr (LOAD) {
           load_step(x + 3, LS);
@@ -353,7 +366,11 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
       using W0 = std::integral_constant<int, 0>;
       // steps 0 and 1 landed (step 2's loads may still fly); publish them
       asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(LOADS) : "memory");
-      if constexpr (NACT > 0) read_frags(0, 0, 0);
+      if constexpr (NACT > 0) {
+#pragma unroll
+        for (int wc = 0; wc < 4; ++wc) wf[wc] = read_w(0, wc);
+        tf[0] = read_t(0, 0);
+      }
       int x = 0;
       for (; x + 4 < nkl; x += 4)
         static_for<4>([&](auto u_c) { step(x + u_c, u_c, T_{}, T_{}, W2{}); });
@@ -373,61 +390,52 @@ __global__ void __launch_bounds__(kThreads, 1) gemm_dense_kernel(GemmProblem p) 
       // [(ridx KS + part) kPartRows + r] 256 + c (same register layout as below)
       float* const dst = reinterpret_cast<float*>(static_cast<char*>(p.dense_part) + kPartMetaBytes) +
                          ((size_t)ridx * KS + part) * (kPartRows * 256);
-      const int h = lane >> 5;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i < nact) {
-          const int r = (wm + 2 * i) * 32 + (lane & 31);  // < kPartRows: at most 6 fragments
+      for (int f = 0; f < 8; ++f) {
+        if ((f >> 1) < nact) {
+          const int r = (wm + 2 * (f >> 1)) * 32 + (f & 1) * 16 + (lane & 15);  // < kPartRows: at most 6 blocks
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              f32x4 v;
-#pragma unroll
-              for (int c = 0; c < 4; ++c) v[c] = acc[i][j][4 * g + c];
-              *reinterpret_cast<f32x4*>(dst + (size_t)r * 256 + wn * 64 + j * 32 + 8 * g + 4 * h) = v;
-            }
+          for (int wc = 0; wc < 4; ++wc)  // columns (wc / 2) * 32 + (wc % 2) * 16 + 4 (lane / 16) + 0..3 of slot wn
+            *reinterpret_cast<f32x4*>(dst + (size_t)r * 256 + wn * 64 + (wc >> 1) * 32 + (wc & 1) * 16 + 4 * (lane >> 4)) =
+                acc[f][wc];
         }
       }
       continue;
     }
-    // ---- epilogue. acc[i][j] is the transposed 32x32 tile (weights were the
-    // first MFMA operand): lane l holds token row (wm + 2 i) * 32 + l % 32 and
-    // weight columns 8 g + 4 (l / 32) + 0..3 of fragment j in registers
-    // 4 g .. 4 g + 3. Those 8-byte runs go into an LDS copy of the output
-    // tile (rows of TCOLS bf16, 16-byte chunks XOR-swizzled by row), which then
-    // leaves in whole rows, one 16-byte chunk per thread, as streaming stores.
+    // ---- epilogue. acc[f][wc] is the transposed 16x16 tile (weights were
+    // the first MFMA operand): lane l holds token row l % 16 of fragment f and
+    // weight columns 4 (l / 16) + 0..3 of fragment wc. Those 8-byte runs go
+    // into an LDS copy of the output tile (rows of TCOLS bf16, 16-byte chunks
+    // XOR-swizzled by row), which then leaves in whole rows, one 16-byte
+    // chunk per thread, as streaming stores.
     {
       constexpr int OCH = TCOLS * 2 / 16;   // 16-byte chunks per output row
       constexpr int OROWS = kThreads / OCH; // rows per store pass
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // every wave is done with the ring
-      const int h = lane >> 5;
+      const int hb = 8 * ((lane >> 4) & 1);  // byte offset of the 4-column run in its 16-byte chunk
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int f = 0; f < 8; ++f) {
         __builtin_amdgcn_sched_barrier(0);
-        if (i < nact) {
-          const int r = (wm + 2 * i) * 32 + (lane & 31);
+        if ((f >> 1) < nact) {
+          const int r = (wm + 2 * (f >> 1)) * 32 + (f & 1) * 16 + (lane & 15);
           char* const orow = smem + r * (TCOLS * 2);
+          if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            if constexpr (EPI == EPI_SWIGLU) {
-              {  // weight slot wn: gate fragment 0, up fragment 1
-                bf16x4 v;
+            for (int q = 0; q < 2; ++q) {  // gate fragment q, up fragment 2 + q: h columns wn * 32 + q * 16 + 4 (l / 16)
+              bf16x4 v;
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
-                  v[c] = static_cast<__bf16>(silu_f(acc[i][0][4 * g + c]) * acc[i][1][4 * g + c]);
-                const int ch = wn * 4 + g;  // h column wn * 32 + 8 g + 4 h
-                *reinterpret_cast<bf16x4*>(orow + ((ch ^ (r & (OCH - 1))) << 4) + 8 * h) = v;
-              }
-            } else {
+              for (int c = 0; c < 4; ++c) v[c] = static_cast<__bf16>(silu_f(acc[f][q][c]) * acc[f][2 + q][c]);
+              const int ch = wn * 4 + q * 2 + (lane >> 5);
+              *reinterpret_cast<bf16x4*>(orow + ((ch ^ (r & (OCH - 1))) << 4) + hb) = v;
+            }
+          } else {
 #pragma unroll
-              for (int j = 0; j < 2; ++j) {  // output column wn * 64 + j * 32 + 8 g + 4 h
-                bf16x4 v;
+            for (int wc = 0; wc < 4; ++wc) {  // output columns wn * 64 + (wc / 2) * 32 + (wc % 2) * 16 + 4 (l / 16)
+              bf16x4 v;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) v[c] = static_cast<__bf16>(acc[i][j][4 * g + c]);
-                const int ch = wn * 8 + j * 4 + g;
-                *reinterpret_cast<bf16x4*>(orow + ((ch ^ (r & (OCH - 1))) << 4) + 8 * h) = v;
-              }
+              for (int c = 0; c < 4; ++c) v[c] = static_cast<__bf16>(acc[f][wc][c]);
+              const int ch = wn * 8 + (wc >> 1) * 4 + (wc & 1) * 2 + (lane >> 5);
+              *reinterpret_cast<bf16x4*>(orow + ((ch ^ (r & (OCH - 1))) << 4) + hb) = v;
             }
           }
         }
