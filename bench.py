@@ -526,6 +526,8 @@ def main():
                     help="whole experts the CPU-oracle baseline runs, the rest of its expert FFN scaled (0: all)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run 3 plain device copies of this many MiB (reference for HBM byte counters)")
+    ap.add_argument("--library-gemm-only", action="store_true",
+                    help="only time the vendor-library reference GEMM1 at the Mixtral shape (for profiling it)")
     ap.add_argument("--ffn-only", action="store_true",
                     help="profiling aid: run only the timed expert-FFN loop of the workload and print its timing")
     args = ap.parse_args()
@@ -540,6 +542,9 @@ def main():
 
     moe.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
+    if args.library_gemm_only:
+        print(json.dumps(dict(library_gemm1=library_gemm_reference(args.steps, args.warmup))))
+        return
     if args.copy_calibration_mb:
         n = args.copy_calibration_mb << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
