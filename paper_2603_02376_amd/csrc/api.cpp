@@ -268,32 +268,46 @@ struct FusedShared {
   void* out = nullptr;
 };
 
+// How run_ffn runs the two GEMMs.
+struct FfnOptions {
+  bool packed = false;                // weights from moe_pack_weights (wu unused): the packed-weight kernels
+  const FusedShared* fused = nullptr;  // packed, same intermediate size: the shared expert over all a_rows
+                                       // tokens rides along as an extra group
+  // 16 tile-queue heads (GEMM1, GEMM2) for the packed path, then (with
+  // one_launch) the one-launch FFN's counters; zeroed here unless
+  // queues_zeroed (moe_layer zeroes them in its dispatch)
+  int32_t* queues = nullptr;
+  bool queues_zeroed = false;
+  const float* x_scales = nullptr;  // x holds int8 codes of rows with these fp32 scales (packed only)
+  bool x_fp8 = false;               // with x_scales: the codes are FP8 (E4M3)
+  // packed only: group g owns rows [offsets[g], seg_end[g]); at most max_wg
+  // workgroups per GEMM (0: one per compute unit)
+  const int32_t* seg_end = nullptr;
+  int32_t max_wg = 0;
+  // the groups hold exactly `rows` rows between them (false for a range of
+  // groups or row segments: the GEMMs then keep the weight-streaming kernel,
+  // whose choice does not depend on the groups' sizes)
+  bool rows_exact = true;
+  // workspace in which the compute-bound GEMM2 may split the K range of
+  // short remainder blocks (nullptr: never)
+  void* dense_part = nullptr;
+  size_t dense_part_bytes = 0;
+  // both weight-streaming GEMMs as one launch when the problem allows it
+  // (bf16 tokens over whole groups, every compute unit), so the end of GEMM1
+  // overlaps the start of GEMM2
+  bool one_launch = false;
+};
+
 // Dense or grouped SwiGLU FFN: h = silu(X Wgᵀ) * (X Wuᵀ) into `h`, then
-// y = h Wdᵀ into `y`. packed: weights from moe_pack_weights (wu unused) and
-// the weight-streaming kernel; fused (packed only, same intermediate size):
-// the shared expert over all a_rows tokens rides along as an extra group.
-// queues: 16 tile-queue heads (GEMM1, GEMM2) for the packed path, then (with
-// one_launch) the one-launch FFN's counters, zeroed here unless queues_zeroed
-// (moe_layer zeroes them in its dispatch).
-// x_scales: x holds int8 codes of rows with these fp32 scales (packed only).
-// seg_end, max_wg (packed only): group g owns rows [offsets[g], seg_end[g]);
-// at most max_wg workgroups per GEMM (0: one per compute unit).
-// rows_exact: the groups hold exactly `rows` rows between them (false for a
-// range of groups or row segments: the GEMMs then keep the weight-streaming
-// kernel, whose choice does not depend on the groups' sizes).
-// dense_part: workspace in which the compute-bound GEMM2 may split the K
-// range of short remainder blocks (nullptr: never).
-// one_launch: run both weight-streaming GEMMs as one launch when the problem
-// allows it (bf16 tokens over whole groups, every compute unit), so the
-// end of GEMM1 overlaps the start of GEMM2.
+// y = h Wdᵀ into `y`.
 hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t groups, int32_t inter, const void* x,
                    const int32_t* gather, const int32_t* offsets, const void* wg, const void* wu, const void* wd,
-                   void* h, void* y, hipStream_t s, bool packed = false, const FusedShared* fused = nullptr,
-                   int32_t* queues = nullptr, const float* x_scales = nullptr, const int32_t* seg_end = nullptr,
-                   int32_t max_wg = 0, bool x_fp8 = false, bool queues_zeroed = false, bool rows_exact = true,
-                   void* dense_part = nullptr, size_t dense_part_bytes = 0, bool one_launch = false) {
-  one_launch = one_launch && packed && queues && !x_scales && !seg_end && max_wg == 0;
-  if (packed && queues && !queues_zeroed) {
+                   void* h, void* y, hipStream_t s, const FfnOptions& o = {}) {
+  const bool packed = o.packed;
+  int32_t* const queues = o.queues;
+  const int32_t* const seg_end = o.seg_end;
+  const bool one_launch = o.one_launch && packed && queues && !o.x_scales && !seg_end && o.max_wg == 0;
+  if (packed && queues && !o.queues_zeroed) {
     const hipError_t e = moe::launch_queue_reset(queues, one_launch ? kRoutedInts : 16, s);
     if (e != hipSuccess) return e;
   }
@@ -310,18 +324,18 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   up.K = c.d;
   up.C = h;
   up.ldc = inter;
-  if (fused && fused->w_gate_up) {
+  if (o.fused && o.fused->w_gate_up) {
     up.xA = x;
-    up.xB = fused->w_gate_up;
-    up.xC = fused->h;
+    up.xB = o.fused->w_gate_up;
+    up.xC = o.fused->h;
     up.x_rows = a_rows;
   }
   up.tile_queue = queues;
-  up.a_scale = x_scales;
-  up.a_fp8 = x_fp8 ? 1 : 0;
+  up.a_scale = o.x_scales;
+  up.a_fp8 = o.x_fp8 ? 1 : 0;
   up.seg_end = seg_end;
-  up.max_wg = max_wg;
-  up.rows_exact = rows_exact && !seg_end ? 1 : 0;
+  up.max_wg = o.max_wg;
+  up.rows_exact = o.rows_exact && !seg_end ? 1 : 0;
   moe::GemmProblem down{};
   down.A = h;
   down.a_rows = rows;
@@ -333,18 +347,18 @@ hipError_t run_ffn(const moe_config_t& c, int32_t a_rows, int32_t rows, int32_t 
   down.K = inter;
   down.C = y;
   down.ldc = c.d;
-  if (fused) {
-    down.xA = fused->h;
-    down.xB = fused->w_down;
-    down.xC = fused->out;
+  if (o.fused) {
+    down.xA = o.fused->h;
+    down.xB = o.fused->w_down;
+    down.xC = o.fused->out;
     down.x_rows = a_rows;
   }
   down.tile_queue = queues ? queues + 8 : nullptr;
   down.seg_end = seg_end;
-  down.max_wg = max_wg;
+  down.max_wg = o.max_wg;
   down.rows_exact = up.rows_exact;
-  down.dense_part = dense_part;
-  down.dense_part_bytes = (int64_t)dense_part_bytes;
+  down.dense_part = o.dense_part;
+  down.dense_part_bytes = (int64_t)o.dense_part_bytes;
   if (one_launch) {
     up.deps = down.deps = queues + 16;
     const hipError_t e = moe::launch_ffn_stream(up, down, s);
@@ -454,9 +468,13 @@ hipError_t run_ffn_segments(const moe_config_t& c, int32_t n_rows, const void* x
   // packed bf16: an expert's gate+up block is 2*I*d elements, its down block d*I
   const char* wgu = static_cast<const char*>(w_gate_up) + (size_t)e0 * 2 * c.I * c.d * 2;
   const char* wd = static_cast<const char*>(w_down) + (size_t)e0 * c.d * c.I * 2;
-  return run_ffn(c, n_rows, n_rows, e1 - e0, c.I, x, nullptr, seg_begin + e0, wgu, nullptr, wd, ws + L.h, y, s, true,
-                 nullptr, reinterpret_cast<int32_t*>(ws + L.queues), nullptr, seg_end ? seg_end + e0 : nullptr,
-                 max_wg, false, false, /*rows_exact=*/false);
+  FfnOptions o;
+  o.packed = true;
+  o.queues = reinterpret_cast<int32_t*>(ws + L.queues);
+  o.seg_end = seg_end ? seg_end + e0 : nullptr;
+  o.max_wg = max_wg;
+  o.rows_exact = false;
+  return run_ffn(c, n_rows, n_rows, e1 - e0, c.I, x, nullptr, seg_begin + e0, wgu, nullptr, wd, ws + L.h, y, s, o);
 }
 
 hipError_t run_ep_copy(const moe_config_t& c, int32_t mode, int32_t n_rows, const void* src, int32_t src_tokens,
@@ -595,11 +613,14 @@ int moe_expert_ffn(const moe_config_t* cfg, int32_t T, const void* x, const int3
   if (T == 0) return MOE_OK;
   clear_pending_error();
   const Layout L = make_layout(*cfg, T);
+  FfnOptions o;
+  o.packed = packed;
+  o.queues = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues);
+  o.dense_part = static_cast<char*>(ws) + L.dense_part;
+  o.dense_part_bytes = L.dense_part_bytes;
+  o.one_launch = true;
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, x, sorted_token, offsets, w_gate, w_up, w_down,
-                               static_cast<char*>(ws) + L.h, y_perm, stream, packed, nullptr,
-                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), nullptr, nullptr, 0,
-                               false, false, true, static_cast<char*>(ws) + L.dense_part, L.dense_part_bytes,
-                               /*one_launch=*/true);
+                               static_cast<char*>(ws) + L.h, y_perm, stream, o);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN");
 }
 
@@ -641,10 +662,13 @@ int moe_expert_ffn_q8(const moe_config_t* cfg, int32_t T, const int8_t* codes, c
   if (T == 0) return MOE_OK;
   clear_pending_error();
   const Layout L = make_layout(*cfg, T);
+  FfnOptions o;
+  o.packed = true;
+  o.queues = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues);
+  o.x_scales = scales;
+  o.x_fp8 = cfg->token_quant == MOE_QUANT_FP8;
   const hipError_t e = run_ffn(*cfg, T, T * cfg->k, cfg->E, cfg->I, codes, sorted_token, offsets, w_gate_up, nullptr,
-                               w_down, static_cast<char*>(ws) + L.h, y_perm, stream, true, nullptr,
-                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues), scales, nullptr, 0,
-                               cfg->token_quant == MOE_QUANT_FP8);
+                               w_down, static_cast<char*>(ws) + L.h, y_perm, stream, o);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "expert FFN (quantized tokens)");
 }
 
@@ -662,9 +686,11 @@ int moe_shared_ffn(const moe_config_t* cfg, int32_t T, const void* x, const void
   if (T == 0) return MOE_OK;
   clear_pending_error();
   const Layout L = make_layout(*cfg, T);
+  FfnOptions o;
+  o.packed = packed;
+  o.queues = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues) + kSharedQueue;
   const hipError_t e = run_ffn(*cfg, T, T, 1, cfg->I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down,
-                               static_cast<char*>(ws) + L.shared_h, out, stream, packed, nullptr,
-                               reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.queues) + kSharedQueue);
+                               static_cast<char*>(ws) + L.shared_h, out, stream, o);
   return e == hipSuccess ? MOE_OK : hip_fail(e, "shared FFN");
 }
 
@@ -738,6 +764,9 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
   const bool fuse_down = packed && c.n_shared && c.I_shared == c.I && q8;
   const bool own = c.n_shared && !fuse && !fuse_down;  // the shared expert as a separate FFN
   const bool two = own && s_aux && s_aux != s_main;
+  FfnOptions shared_opts;  // the shared expert as its own FFN
+  shared_opts.packed = packed;
+  shared_opts.queues = queues + kSharedQueue;
   StreamEvents* ev = nullptr;
   if (two) {
     // fork: the shared expert on s_aux may start once x is ready on s_main
@@ -745,7 +774,7 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     if ((e = hipEventRecord(ev->fork, s_main)) != hipSuccess) return hip_fail(e, "event record");
     if ((e = hipStreamWaitEvent(s_aux, ev->fork, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h, shared,
-                     s_aux, packed, nullptr, queues + kSharedQueue)) != hipSuccess)
+                     s_aux, shared_opts)) != hipSuccess)
       return hip_fail(e, "shared FFN");
     if ((e = hipEventRecord(ev->join, s_aux)) != hipSuccess) return hip_fail(e, "event record");
   }
@@ -782,17 +811,24 @@ int moe_layer(const moe_config_t* cfg, int32_t T, const void* x, const void* w_r
     g.tile_queue = queues + kSharedQueue;
     if ((e = moe::launch_gemm_stream(g, moe::EPI_SWIGLU, s_main)) != hipSuccess) return hip_fail(e, "shared GEMM1");
   }
+  FfnOptions routed;
+  routed.packed = packed;
+  routed.fused = (fuse || fuse_down) ? &fs : nullptr;
+  routed.queues = queues;
+  routed.queues_zeroed = true;  // by the dispatch
+  routed.x_scales = q8 ? qscales : nullptr;
+  routed.x_fp8 = f8;
+  routed.dense_part = w + L.dense_part;
+  routed.dense_part_bytes = L.dense_part_bytes;
+  routed.one_launch = true;
   if ((e = run_ffn(c, T, T * c.k, c.E, c.I, q8 ? static_cast<const void*>(qcodes) : x, st, offsets, w_gate, w_up,
-                   w_down, w + L.h, y, s_main, packed, (fuse || fuse_down) ? &fs : nullptr, queues,
-                   q8 ? qscales : nullptr, nullptr, 0, f8, /*queues_zeroed=*/true, /*rows_exact=*/true,
-                   w + L.dense_part, L.dense_part_bytes, /*one_launch=*/true)) !=
-      hipSuccess)
+                   w_down, w + L.h, y, s_main, routed)) != hipSuccess)
     return hip_fail(e, "expert FFN");
   if (own) {
     if (two) {
       if ((e = hipStreamWaitEvent(s_main, ev->join, 0)) != hipSuccess) return hip_fail(e, "stream wait");
     } else if ((e = run_ffn(c, T, T, 1, c.I_shared, x, nullptr, nullptr, ws_gate, ws_up, ws_down, w + L.shared_h,
-                            shared, s_main, packed, nullptr, queues + kSharedQueue)) != hipSuccess) {
+                            shared, s_main, shared_opts)) != hipSuccess) {
       return hip_fail(e, "shared FFN");
     }
   }
