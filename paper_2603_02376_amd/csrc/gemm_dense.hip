@@ -27,9 +27,9 @@
 //     side so the fragment reads are bank-conflict free.
 //   * At the end of step x every wave waits for its own loads of step x+2 and
 //     meets the others at one barrier, which publishes step x+2 and frees the
-//     slot read in step x; the first K slice of step x+1 (published a step
-//     earlier) is read before that barrier, so no LDS latency sits between a
-//     barrier and the MFMAs. Only direct loads write the ring during the K
+//     slot read in step x; the first token fragment and the weight fragments
+//     of step x+1 (published a step earlier) are read before that barrier, so
+//     no LDS latency sits between a barrier and the MFMAs. Only direct loads write the ring during the K
 //     loop, so the hand-written vmcnt waits are exact.
 //   * Rows: an expert's segment is cut into full 256-row blocks plus one
 //     remainder block; 32-row fragments alternate between the two wave rows,
