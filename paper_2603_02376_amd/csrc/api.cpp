@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <map>
 #include <mutex>
 #include <string>
 
@@ -511,6 +512,21 @@ int device_cu_count() {
     cache[dev] = n;
   }
   return cache[dev];
+}
+
+hipError_t set_dynamic_lds(const void* kern, int bytes) {
+  static std::mutex mu;
+  static std::map<std::pair<const void*, int>, hipError_t> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_pair(kern, dev);
+  const auto it = done.find(key);
+  if (it != done.end()) return it->second;
+  e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  done.emplace(key, e);
+  return e;
 }
 
 }  // namespace moe

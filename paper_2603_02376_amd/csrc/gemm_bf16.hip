@@ -384,17 +384,14 @@ template <int BM, int BN, int BK, int WGM, int WGN, int EPI, bool OUT_F32>
 hipError_t launch_cfg(const GemmProblem& p, hipStream_t s) {
   auto kern = gemm_bf16_kernel<BM, BN, BK, WGM, WGN, EPI, OUT_F32>;
   constexpr size_t lds = kLdsRing;
-  static std::once_flag once;
-  static int occ = 1;
-  static hipError_t init_err = hipSuccess;
-  std::call_once(once, [&] {
-    init_err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (init_err == hipSuccess) {
-      int o = 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, kern, 64 * WGM * WGN, lds) == hipSuccess && o > 0) occ = o;
-    }
-  });
+  const hipError_t init_err = set_dynamic_lds((const void*)kern, (int)lds);
   if (init_err != hipSuccess) return init_err;
+  static std::once_flag once;  // the occupancy is the same on every gfx950 device
+  static int occ = 1;
+  std::call_once(once, [&] {
+    int o = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, kern, 64 * WGM * WGN, lds) == hipSuccess && o > 0) occ = o;
+  });
   const int ncols_tile = (EPI == EPI_SWIGLU) ? BN / 2 : BN;
   const long long nt = (p.N + ncols_tile - 1) / ncols_tile;
   const int groups = p.offsets ? p.groups : 1;

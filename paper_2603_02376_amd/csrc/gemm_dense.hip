@@ -45,7 +45,6 @@
 #include "moe_internal.h"
 
 #include <algorithm>
-#include <mutex>
 #include <type_traits>
 #include <utility>
 
@@ -492,11 +491,7 @@ size_t part_need(int groups, int nt) {
 template <int EPI>
 hipError_t launch_dense(const GemmProblem& p, hipStream_t s) {
   auto kern = gemm_dense_kernel<EPI>;
-  static std::once_flag once;
-  static hipError_t init_err = hipSuccess;
-  std::call_once(once, [&] {
-    init_err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kRing);
-  });
+  const hipError_t init_err = set_dynamic_lds((const void*)kern, kRing);
   if (init_err != hipSuccess) return init_err;
   const int tcols = (EPI == EPI_SWIGLU) ? 128 : 256;
   const int groups = p.offsets ? p.groups : 1;

@@ -67,7 +67,6 @@
 #include "moe_internal.h"
 
 #include <algorithm>
-#include <mutex>
 #include <type_traits>
 #include <utility>
 
@@ -770,11 +769,7 @@ hipError_t launch_stream(const GemmProblem& p, hipStream_t s) {
   constexpr int kMaxRows = StreamCfg<DEEP>::rows, kSlots = StreamCfg<DEEP>::slots;
   constexpr size_t lds = std::max<size_t>((size_t)kSlots * kMaxRows * 128,
                                           (size_t)kMaxRows * ((EPI == EPI_SWIGLU) ? 128 : 256) * 2);
-  static std::once_flag once;
-  static hipError_t init_err = hipSuccess;
-  std::call_once(once, [&] {
-    init_err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  });
+  const hipError_t init_err = set_dynamic_lds((const void*)kern, (int)lds);
   if (init_err != hipSuccess) return init_err;
   // A is addressed through a buffer resource: 32-bit byte offsets.
   if ((size_t)p.a_rows * (size_t)p.K * (Q8 ? 1 : 2) > 0xFFFFFFFFull || (size_t)p.x_rows * (size_t)p.K * 2 > 0xFFFFFFFFull)
@@ -829,11 +824,7 @@ hipError_t launch_ffn(const GemmProblem& up, const GemmProblem& down, long long 
   constexpr size_t lds2 = std::max<size_t>((size_t)StreamCfg<DEEP2>::slots * StreamCfg<DEEP2>::rows * 128,
                                            (size_t)StreamCfg<DEEP2>::rows * 256 * 2);
   constexpr size_t lds = std::max(lds1, lds2);
-  static std::once_flag once;
-  static hipError_t init_err = hipSuccess;
-  std::call_once(once, [&] {
-    init_err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  });
+  const hipError_t init_err = set_dynamic_lds((const void*)kern, (int)lds);
   if (init_err != hipSuccess) return init_err;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, s, up, down);
   return hipGetLastError();

@@ -232,5 +232,9 @@ hipError_t launch_ep_plan(const EpPlanParams& p, hipStream_t s);
 
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
+// Raises kernel `kern`'s dynamic LDS limit to `bytes` on the current device,
+// once per (kernel, device): the attribute belongs to the device's copy of the
+// kernel. Later calls return the first call's status.
+hipError_t set_dynamic_lds(const void* kern, int bytes);
 
 }  // namespace moe
