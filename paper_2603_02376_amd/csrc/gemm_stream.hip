@@ -439,7 +439,7 @@ __device__ __forceinline__ void stream_gemm(const GemmProblem& p, char* smem, St
     // next to it and find its weights there); otherwise non-temporal loads
     // (weights read once).
     auto body = [&](auto ar_c, auto temporal_c) __attribute__((always_inline)) {
-      constexpr int AR = decltype(ar_c)::value;  // A rows staged per step (128 or kMaxRows)
+      constexpr int AR = decltype(ar_c)::value;  // A rows staged per step (32, 128 or kMaxRows)
       constexpr bool TEMPORAL = decltype(temporal_c)::value;
       constexpr int A_CH = Q8 ? AR / (16 * kWaves) : AR / (8 * kWaves);  // A loads per wave per step
       constexpr int LOADS = A_CH + 8;
@@ -611,7 +611,18 @@ __device__ __forceinline__ void stream_gemm(const GemmProblem& p, char* smem, St
       // passes has at least 3.
       with_count_from<AR / 32, (AR > 128 ? 5 : (TEMPORAL ? 3 : 0))>(min(nact, AR / 32), kloop);
     };
-    if (rows <= 128) {
+    // A single pass of at most 32 rows stages one 32-row fragment: one token-row
+    // load per wave and step instead of four copies of its last row
+    // (bf16 tokens; a 32-row block of 1-byte codes would be half a load).
+    bool thin = false;
+    if constexpr (!Q8) {
+      if (rows <= 32 && !multi) {
+        body(std::integral_constant<int, 32>{}, std::false_type{});
+        thin = true;
+      }
+    }
+    if (thin) {
+    } else if (rows <= 128) {
       if (multi) body(std::integral_constant<int, 128>{}, std::true_type{});
       else body(std::integral_constant<int, 128>{}, std::false_type{});
     } else if (multi) body(std::integral_constant<int, kMaxRows>{}, std::true_type{});
