@@ -50,8 +50,9 @@
  *  - Calls that share one workspace must not overlap in time.
  *  - Calls enqueue kernels and (moe_layer with s_aux, moe_ep_expert_ffn)
  *    event records and waits only: no allocation, copy, memset or host
- *    synchronisation. A call (after one eager call of it in the process,
- *    which sets up the kernels' attributes and the calling thread's events)
+ *    synchronisation. A call (after one eager call of it on the device from
+ *    the capturing thread, which sets up the kernels' attributes on that
+ *    device and the thread's events)
  *    may therefore be captured in a HIP graph; each replay reads the
  *    buffers' contents at replay time (moe_layer's replays are tested to
  *    give the bits of eager calls).
